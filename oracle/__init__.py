@@ -1,0 +1,190 @@
+"""CPU oracle for Elastic Shadow Pricing -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The HIP library and its Python binding
+never import it; the two share no code.
+
+A thin ctypes layer over ``esp_oracle.c`` (plain single-threaded C, fp64,
+``-ffp-contract=off``), which follows the paper's Sec. 3.2 (Eq. 6-8): per-job
+argmax of utility minus price-weighted demand, exact aggregate demand, and the
+projected-subgradient price update.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "esp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle_esp.so")
+
+CFLAGS = ["-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+          "-Wall", "-Wextra"]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle library with gcc (x86-64 SSE2 binary64, no contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.run(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Problem(C.Structure):
+    _fields_ = [
+        ("B", C.c_int32), ("N", C.c_int32), ("R", C.c_int32), ("nnz", C.c_int64),
+        ("offsets", C.c_void_p), ("utility", C.c_void_p), ("demand", C.c_void_p),
+        ("feasible", C.c_void_p), ("capacity", C.c_void_p), ("eta0", C.c_void_p),
+        ("rule", C.c_int32),
+    ]
+
+
+_lib = None
+
+
+def bind(path: str):
+    """Load an oracle library build and declare its signatures."""
+    L = C.CDLL(path)
+    _declare(L)
+    return L
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        _lib = bind(_LIB)
+    return _lib
+
+
+def _declare(L):
+    vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
+    L.orc_exact_sum_f32.argtypes = [vp, i64]
+    L.orc_exact_sum_f32.restype = dbl
+    L.orc_score.argtypes = [vp, C.c_int, i64, vp]
+    L.orc_score.restype = dbl
+    L.orc_select.argtypes = [vp, C.c_int, vp, vp]
+    L.orc_select.restype = None
+    L.orc_demand.argtypes = [vp, C.c_int, vp, vp]
+    L.orc_demand.restype = None
+    L.orc_eta.argtypes = [C.c_int, dbl, i64]
+    L.orc_eta.restype = dbl
+    L.orc_update.argtypes = [C.c_int, vp, vp, dbl, vp]
+    L.orc_update.restype = None
+    L.orc_dual_value.argtypes = [vp, C.c_int, vp, vp]
+    L.orc_dual_value.restype = dbl
+    L.orc_primal_value.argtypes = [vp, C.c_int, vp]
+    L.orc_primal_value.restype = dbl
+    L.orc_solve.argtypes = [vp, vp, i32, i32, dbl, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.orc_solve.restype = C.c_int
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def exact_sum_f32(values, L=None) -> float:
+    """Exact sum of non-negative float32 values, rounded once to float64."""
+    v = np.ascontiguousarray(values, dtype=np.float32)
+    return float((L or lib()).orc_exact_sum_f32(_p(v), v.size))
+
+
+def eta(rule: int, eta0: float, t: int, L=None) -> float:
+    return float((L or lib()).orc_eta(rule, eta0, t))
+
+
+def update(U, Cap, eta_t: float, lam, L=None) -> np.ndarray:
+    U = np.ascontiguousarray(U, dtype=np.float64)
+    Cap = np.ascontiguousarray(Cap, dtype=np.float64)
+    out = np.array(lam, dtype=np.float64, copy=True)
+    (L or lib()).orc_update(out.size, _p(U), _p(Cap), eta_t, _p(out))
+    return out
+
+
+class Oracle:
+    """Oracle bound to one logical instance (a ``workloads.Instance`` or any
+    object with the same fields)."""
+
+    def __init__(self, inst, L=None):
+        self.L = L or lib()
+        self.inst = inst
+        self.offsets = np.ascontiguousarray(inst.offsets, dtype=np.int64)
+        self.utility = np.ascontiguousarray(inst.utility, dtype=np.float32)
+        self.demand = np.ascontiguousarray(inst.demand, dtype=np.float32)
+        self.capacity = np.ascontiguousarray(inst.capacity, dtype=np.float64)
+        self.eta0 = np.ascontiguousarray(inst.eta0, dtype=np.float64)
+        self.feasible = (None if inst.feasible is None
+                         else np.ascontiguousarray(inst.feasible, dtype=np.uint8))
+        self.B, self.N, self.R = self.utility.shape[0], self.offsets.size - 1, self.demand.shape[2]
+        self.rule = int(inst.rule)
+        self._prob = _Problem(self.B, self.N, self.R, int(self.offsets[-1]),
+                              _p(self.offsets), _p(self.utility), _p(self.demand),
+                              _p(self.feasible), _p(self.capacity), _p(self.eta0), self.rule)
+        self._pp = C.addressof(self._prob)
+
+    # single steps -------------------------------------------------------
+    def score(self, b: int, e: int, lam) -> float:
+        lam = np.ascontiguousarray(lam, dtype=np.float64)
+        return float(self.L.orc_score(self._pp, b, e, _p(lam)))
+
+    def select(self, b: int, lam) -> np.ndarray:
+        lam = np.ascontiguousarray(lam, dtype=np.float64)
+        ch = np.empty(self.N, dtype=np.int32)
+        self.L.orc_select(self._pp, b, _p(lam), _p(ch))
+        return ch
+
+    def demand_sum(self, b: int, choice) -> np.ndarray:
+        ch = np.ascontiguousarray(choice, dtype=np.int32)
+        U = np.empty(self.R, dtype=np.float64)
+        self.L.orc_demand(self._pp, b, _p(ch), _p(U))
+        return U
+
+    def eta(self, b: int, t: int) -> float:
+        return eta(self.rule, float(self.eta0[b]), t, self.L)
+
+    def step(self, b: int, lam, t: int):
+        """One iteration at lambda^t: (choice c^t, U^t, lambda^{t+1})."""
+        ch = self.select(b, lam)
+        U = self.demand_sum(b, ch)
+        return ch, U, update(U, self.capacity[b], self.eta(b, t), lam, self.L)
+
+    def dual_value(self, b: int, lam, choice) -> float:
+        lam = np.ascontiguousarray(lam, dtype=np.float64)
+        ch = np.ascontiguousarray(choice, dtype=np.int32)
+        return float(self.L.orc_dual_value(self._pp, b, _p(lam), _p(ch)))
+
+    def primal_value(self, b: int, choice) -> float:
+        ch = np.ascontiguousarray(choice, dtype=np.int32)
+        return float(self.L.orc_primal_value(self._pp, b, _p(ch)))
+
+    # whole loop ---------------------------------------------------------
+    def solve(self, lam0=None, iters: Optional[int] = None, t_start: int = 1, tol: float = 0.0,
+              trace: bool = True, trace_choice: bool = False) -> dict:
+        T = int(self.inst.iters if iters is None else iters)
+        B, N, R = self.B, self.N, self.R
+        lam = np.array(self.inst.lam0 if lam0 is None else lam0, dtype=np.float64).reshape(B, R).copy()
+        out = {
+            "choice": np.empty((B, N), dtype=np.int32),
+            "U": np.empty((B, R), dtype=np.float64),
+            "iters_done": np.empty(B, dtype=np.int32),
+        }
+        if trace:
+            out["tr_lam"] = np.full((T, B, R), np.nan)
+            out["tr_U"] = np.full((T, B, R), np.nan)
+            out["tr_dual"] = np.full((T, B), np.nan)
+            out["tr_primal"] = np.full((T, B), np.nan)
+        if trace_choice:
+            out["tr_choice"] = np.full((T, B, N), -1, dtype=np.int32)
+        rc = self.L.orc_solve(self._pp, _p(lam), T, t_start, tol,
+                             _p(out.get("tr_lam")), _p(out.get("tr_U")), _p(out.get("tr_choice")),
+                             _p(out.get("tr_dual")), _p(out.get("tr_primal")),
+                             _p(out["choice"]), _p(out["U"]), _p(out["iters_done"]))
+        if rc != 0:
+            raise ValueError(f"oracle: a job family has no allowed configuration (rc={rc})")
+        out["lam"] = lam
+        return out

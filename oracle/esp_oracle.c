@@ -1,0 +1,276 @@
+/*
+ * CPU oracle for Elastic Shadow Pricing (ESP) -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only the tests, the smoke check and the bench's CPU-baseline leg may load
+ * this file's library.  The product path (the HIP library) never calls it and
+ * shares no code with it.
+ *
+ * Plain, slow, single-threaded C, fp64 arithmetic, built with
+ * -O2 -ffp-contract=off -fno-fast-math on x86-64 (SSE2, no x87, no FMA), so
+ * every + - * / sqrt below is one correctly rounded IEEE-754 binary64 operation
+ * in the order written.
+ *
+ * What it computes (paper Sec. 3.2, "Elastic Shadow Pricing"):
+ *   - the per-job subproblem of the Lagrangian decomposition (Sec. 3.2.2,
+ *     Eq. 6): for fixed prices lambda, job j picks
+ *         c_j = argmax_k [ u_jk - sum_r lambda_r d_jkr ]
+ *     by enumerating its family, lowest index winning ties;
+ *   - the aggregate demand U_r = sum_j d_{j,c_j,r} of the current selection
+ *     (Sec. 3.2.3, definition under Eq. 8), as the exact real sum rounded once
+ *     to binary64 (round-to-nearest-even);
+ *   - the projected-subgradient price update of Eq. 8,
+ *         lambda_r <- max(0, lambda_r + eta_t (U_r - C_r)),
+ *     eta_t = eta0 (fixed) or eta0 / sqrt(t) (diminishing), t = 1, 2, ...;
+ *   - the loop of the tatonnement (Sec. 3.2.2/3.2.3; Alg. 1 "EspTatonnement"
+ *     followed by the per-job re-selection at the final prices);
+ *   - for the pins only: the Lagrangian dual value g(lambda) of Eq. 6 at the
+ *     selected configurations and the primal value sum_j u_{j,c_j} (Eq. 1).
+ *
+ * Readings where the paper is silent (each listed in the design notes):
+ *   score    rent = d0*l0; rent = rent + d_r*l_r (r = 1..R-1); s = u - rent,
+ *            table values widened exactly from fp32 to fp64;
+ *   ties     the lowest configuration index wins (strict '>' scan);
+ *   t        1-based within one solve; a warm start passes t_start;
+ *   project  x > 0 ? x : +0.0 (a stored price is never -0.0);
+ *   Eq. 4    configurations with feasible[e] == 0 are never selected;
+ *   stop     optional: after the update of iteration t, stop when every r has
+ *            |lambda^{t+1}_r - lambda^t_r| <= tol * max(1, lambda^t_r).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "esp_oracle.h"
+
+/* ------------------------------------------------------------------------ */
+/* Exact sum of non-negative binary32 values, rounded once to binary64.       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Every finite binary32 value v >= 0 is an integer multiple of 2^-149, and
+ * v * 2^(149+24) is an integer below 2^(128+173) = 2^301.  The accumulator
+ * holds that integer for the running sum in 32-bit digits, each kept in a
+ * 64-bit word so that digits can absorb up to 2^31 additions before carries
+ * are propagated.  ORC_WORDS * 32 = 384 bits >= 301 + 31 bits of growth.
+ */
+#define ORC_WORDS 12
+#define ORC_BIAS 173   /* integer = value * 2^ORC_BIAS */
+
+typedef struct { uint64_t w[ORC_WORDS]; } orc_acc;
+
+static void acc_clear(orc_acc *a) { memset(a, 0, sizeof(*a)); }
+
+static void acc_add_f32(orc_acc *a, float v)
+{
+    int e;
+    float f;
+    uint64_t mant, chunk;
+    int pos;
+    if (v == 0.0f) return;                 /* +0 and -0 add nothing */
+    f = frexpf(v, &e);                     /* v = f * 2^e, 0.5 <= f < 1 */
+    mant = (uint64_t)ldexpf(f, 24);        /* exact: f has <= 24 significant bits */
+    pos = e - 24 + ORC_BIAS;               /* v * 2^BIAS = mant * 2^pos, pos >= 0 */
+    chunk = mant << (pos % 32);            /* <= 24 + 31 = 55 bits */
+    a->w[pos / 32] += chunk & 0xffffffffu;
+    a->w[pos / 32 + 1] += chunk >> 32;
+}
+
+static void acc_normalize(orc_acc *a)
+{
+    int i;
+    for (i = 0; i + 1 < ORC_WORDS; i++) {
+        a->w[i + 1] += a->w[i] >> 32;
+        a->w[i] &= 0xffffffffu;
+    }
+}
+
+static int acc_bit(const orc_acc *a, int i) { return (int)((a->w[i / 32] >> (i % 32)) & 1u); }
+
+/* Round the accumulated integer * 2^-BIAS to the nearest binary64, ties to even. */
+static double acc_to_double(orc_acc *a)
+{
+    int top = -1, i;
+    uint64_t m = 0;
+    int guard, sticky = 0;
+    acc_normalize(a);
+    for (i = ORC_WORDS * 32 - 1; i >= 0; i--)
+        if (acc_bit(a, i)) { top = i; break; }
+    if (top < 0) return 0.0;
+    if (top <= 52) {                       /* fits in 53 bits: exact */
+        for (i = top; i >= 0; i--) m = (m << 1) | (uint64_t)acc_bit(a, i);
+        return ldexp((double)m, -ORC_BIAS);
+    }
+    for (i = top; i >= top - 52; i--) m = (m << 1) | (uint64_t)acc_bit(a, i);
+    guard = acc_bit(a, top - 53);
+    for (i = top - 54; i >= 0; i--) sticky |= acc_bit(a, i);
+    if (guard && (sticky || (m & 1u))) m += 1;   /* m may become 2^53: still exact */
+    return ldexp((double)m, top - 52 - ORC_BIAS);
+}
+
+double orc_exact_sum_f32(const float *v, int64_t n)
+{
+    orc_acc a;
+    int64_t i;
+    acc_clear(&a);
+    for (i = 0; i < n; i++) acc_add_f32(&a, v[i]);
+    return acc_to_double(&a);
+}
+
+/* ------------------------------------------------------------------------ */
+/* The method.                                                               */
+/* ------------------------------------------------------------------------ */
+
+static const float *util_of(const orc_problem *p, int b) { return p->utility + (int64_t)b * p->nnz; }
+static const float *dem_of(const orc_problem *p, int b) { return p->demand + (int64_t)b * p->nnz * p->R; }
+
+/* Score of table entry e at prices lam (Sec. 3.2.2, the bracket of Eq. 6). */
+double orc_score(const orc_problem *p, int b, int64_t e, const double *lam)
+{
+    const float *d = dem_of(p, b) + e * p->R;
+    double rent = (double)d[0] * lam[0];
+    int r;
+    for (r = 1; r < p->R; r++) rent = rent + (double)d[r] * lam[r];
+    return (double)util_of(p, b)[e] - rent;
+}
+
+static int entry_allowed(const orc_problem *p, int b, int64_t e)
+{
+    return p->feasible == NULL || p->feasible[(int64_t)b * p->nnz + e] != 0;
+}
+
+/* Per-job argmax (Sec. 3.2.2): choice[j] = family index k, lowest k on ties. */
+void orc_select(const orc_problem *p, int b, const double *lam, int32_t *choice)
+{
+    int64_t j;
+    for (j = 0; j < p->N; j++) {
+        int64_t lo = p->offsets[j], hi = p->offsets[j + 1], e;
+        int32_t best_k = -1;
+        double best = 0.0;
+        for (e = lo; e < hi; e++) {
+            double s;
+            if (!entry_allowed(p, b, e)) continue;
+            s = orc_score(p, b, e, lam);
+            if (best_k < 0 || s > best) { best = s; best_k = (int32_t)(e - lo); }
+        }
+        choice[j] = best_k;                 /* -1 only for a family with no allowed entry */
+    }
+}
+
+/* U_r = sum_j d_{j, c_j, r} (Sec. 3.2.3), exact sum rounded once. */
+void orc_demand(const orc_problem *p, int b, const int32_t *choice, double *U)
+{
+    const float *d = dem_of(p, b);
+    int r;
+    for (r = 0; r < p->R; r++) {
+        orc_acc a;
+        int64_t j;
+        acc_clear(&a);
+        for (j = 0; j < p->N; j++) {
+            if (choice[j] < 0) continue;
+            acc_add_f32(&a, d[(p->offsets[j] + choice[j]) * p->R + r]);
+        }
+        U[r] = acc_to_double(&a);
+    }
+}
+
+/* Step size of Eq. 8: fixed eta0, or eta0 / sqrt(t). */
+double orc_eta(int rule, double eta0, int64_t t)
+{
+    if (rule == ORC_STEP_INV_SQRT) return eta0 / sqrt((double)t);
+    return eta0;
+}
+
+/* Projected subgradient step of Eq. 8, in place. */
+void orc_update(int R, const double *U, const double *C, double eta, double *lam)
+{
+    int r;
+    for (r = 0; r < R; r++) {
+        double g = U[r] - C[r];
+        double x = lam[r] + eta * g;
+        lam[r] = (x > 0.0) ? x : 0.0;
+    }
+}
+
+/* Lagrangian (Eq. 6) at the selection: sum_j s_{j,c_j} + sum_r lam_r C_r. */
+double orc_dual_value(const orc_problem *p, int b, const double *lam, const int32_t *choice)
+{
+    double v = 0.0;
+    int64_t j;
+    int r;
+    for (j = 0; j < p->N; j++)
+        if (choice[j] >= 0) v = v + orc_score(p, b, p->offsets[j] + choice[j], lam);
+    for (r = 0; r < p->R; r++) v = v + lam[r] * p->capacity[(int64_t)b * p->R + r];
+    return v;
+}
+
+/* Objective of Eq. 1 at the selection: sum_j u_{j,c_j}. */
+double orc_primal_value(const orc_problem *p, int b, const int32_t *choice)
+{
+    double v = 0.0;
+    int64_t j;
+    for (j = 0; j < p->N; j++)
+        if (choice[j] >= 0) v = v + (double)util_of(p, b)[p->offsets[j] + choice[j]];
+    return v;
+}
+
+/*
+ * The tatonnement for every cluster b (independently):
+ *   for t = t_start .. t_start+T-1:
+ *       select at lambda^t, sum demand U^t, update to lambda^{t+1} (Eq. 8)
+ *   then re-select at the final prices (Alg. 1 after EspTatonnement).
+ * lam [B][R] holds lambda^{t_start} on entry and the final prices on exit.
+ * Optional outputs (NULL to skip), iteration-major:
+ *   tr_lam [T][B][R] lambda^{t+1};  tr_U [T][B][R] U^t;
+ *   tr_choice [T][B][N] c^t;  tr_dual [T][B] g at (lambda^t, c^t);
+ *   tr_primal [T][B] Eq. 1 value of c^t;
+ *   choice_out [B][N], U_out [B][R] at the final prices;
+ *   iters_done [B] number of updates made (< T only with tol > 0).
+ * Returns 0, or -1 when a family has no allowed entry.
+ */
+int orc_solve(const orc_problem *p, double *lam, int32_t T, int32_t t_start, double tol,
+              double *tr_lam, double *tr_U, int32_t *tr_choice, double *tr_dual,
+              double *tr_primal, int32_t *choice_out, double *U_out, int32_t *iters_done)
+{
+    int R = p->R, b, r;
+    int32_t *ch = (int32_t *)malloc(sizeof(int32_t) * (size_t)(p->N > 0 ? p->N : 1));
+    double U[ORC_MAX_R], prev[ORC_MAX_R];
+    int status = 0;
+    if (ch == NULL) return -2;
+    for (b = 0; b < p->B; b++) {
+        double *lb = lam + (int64_t)b * R;
+        const double *Cb = p->capacity + (int64_t)b * R;
+        int32_t i, done = 0;
+        for (i = 0; i < T; i++) {
+            int64_t t = (int64_t)t_start + i;
+            double eta;
+            int conv = 1;
+            orc_select(p, b, lb, ch);
+            orc_demand(p, b, ch, U);
+            if (tr_dual) tr_dual[(int64_t)i * p->B + b] = orc_dual_value(p, b, lb, ch);
+            if (tr_primal) tr_primal[(int64_t)i * p->B + b] = orc_primal_value(p, b, ch);
+            if (tr_choice) memcpy(tr_choice + ((int64_t)i * p->B + b) * p->N, ch, sizeof(int32_t) * (size_t)p->N);
+            eta = orc_eta(p->rule, p->eta0[b], t);
+            for (r = 0; r < R; r++) prev[r] = lb[r];
+            orc_update(R, U, Cb, eta, lb);
+            if (tr_lam) memcpy(tr_lam + ((int64_t)i * p->B + b) * R, lb, sizeof(double) * (size_t)R);
+            if (tr_U) memcpy(tr_U + ((int64_t)i * p->B + b) * R, U, sizeof(double) * (size_t)R);
+            done = i + 1;
+            if (tol > 0.0) {
+                for (r = 0; r < R; r++) {
+                    double diff = fabs(lb[r] - prev[r]);
+                    double scale = prev[r] > 1.0 ? prev[r] : 1.0;
+                    if (!(diff <= tol * scale)) conv = 0;
+                }
+                if (conv) break;
+            }
+        }
+        if (iters_done) iters_done[b] = done;
+        orc_select(p, b, lb, ch);
+        for (i = 0; i < p->N; i++) if (ch[i] < 0) status = -1;
+        if (choice_out) memcpy(choice_out + (int64_t)b * p->N, ch, sizeof(int32_t) * (size_t)p->N);
+        if (U_out) orc_demand(p, b, ch, U_out + (int64_t)b * R);
+    }
+    free(ch);
+    return status;
+}

@@ -1,0 +1,106 @@
+"""Test helpers: golden-fixture parsing, brute-force optimum, LP bound.
+
+None of this is the method: brute force enumerates Eq. 1-3 directly and the LP
+is the continuous relaxation of Eq. 1-3 solved by SciPy's HiGHS.
+"""
+from __future__ import annotations
+
+import itertools
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import workloads
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def read_golden(name: str) -> dict:
+    """Parse a golden text fixture: 'key v1 v2 ...' lines, '|' groups, '#' comments."""
+    out: dict = {"trace": []}
+    with open(os.path.join(GOLDEN, name)) as f:
+        for ln in f:
+            ln = ln.split("#", 1)[0].strip()
+            if not ln:
+                continue
+            key, _, rest = ln.partition(" ")
+            if key == "trace":
+                out["trace"].append([[float(x) for x in g.split()] for g in rest.split("|")])
+            elif "|" in rest:
+                out[key] = [[float(x) for x in g.split()] for g in rest.split("|")]
+            else:
+                vals = rest.split()
+                try:
+                    out[key] = [float(x) for x in vals]
+                except ValueError:
+                    out[key] = vals
+    return out
+
+
+def golden_instance(g: dict) -> workloads.Instance:
+    offsets = np.array(g["offsets"], dtype=np.int64)
+    nnz = int(offsets[-1])
+    util = np.array(g["utility"], dtype=np.float32).reshape(1, nnz)
+    dem = np.array(g["demand"], dtype=np.float32).reshape(1, nnz, -1)
+    R = dem.shape[2]
+    cap = np.array(g["capacity"], dtype=np.float64).reshape(1, R)
+    rule = workloads.STEP_CONST if g["rule"] == ["const"] else workloads.STEP_INV_SQRT
+    lam0 = np.array(g.get("lam0", [0.0] * R), dtype=np.float64).reshape(1, R)
+    return workloads.Instance("golden", 0, offsets, util, dem, cap,
+                              np.array(g["eta0"], dtype=np.float64), rule, lam0, int(g["iters"][0]))
+
+
+def brute_force_optimum(inst: workloads.Instance, b: int = 0):
+    """max sum_j u_{j,c_j} over all selections with sum_j d_{j,c_j} <= C
+    (Eq. 1-3), in exact rational arithmetic.  Returns (P*, argmax tuple) or
+    (None, None) when no selection is feasible."""
+    off = inst.offsets
+    N, R = inst.N, inst.R
+    fam = [range(int(off[j + 1] - off[j])) for j in range(N)]
+    u = [[Fraction(float(inst.utility[b, off[j] + k])) for k in fam[j]] for j in range(N)]
+    d = [[[Fraction(float(inst.demand[b, off[j] + k, r])) for r in range(R)] for k in fam[j]]
+         for j in range(N)]
+    cap = [Fraction(float(c)) for c in inst.capacity[b]]
+    allowed = None if inst.feasible is None else inst.feasible[b]
+    best, arg = None, None
+    for combo in itertools.product(*fam):
+        if allowed is not None and any(allowed[off[j] + k] == 0 for j, k in enumerate(combo)):
+            continue
+        ok = True
+        for r in range(R):
+            if sum(d[j][k][r] for j, k in enumerate(combo)) > cap[r]:
+                ok = False
+                break
+        if not ok:
+            continue
+        v = sum(u[j][k] for j, k in enumerate(combo))
+        if best is None or v > best:
+            best, arg = v, combo
+    return best, arg
+
+
+def lp_optimum(inst: workloads.Instance, b: int = 0) -> float:
+    """Continuous relaxation of Eq. 1-3 (x_jk in [0,1], sum_k x_jk = 1),
+    solved by scipy.optimize.linprog with the HiGHS method."""
+    from scipy.optimize import linprog
+    off = inst.offsets
+    N, R, nnz = inst.N, inst.R, inst.nnz
+    c = -inst.utility[b].astype(np.float64)
+    A_eq = np.zeros((N, nnz))
+    for j in range(N):
+        A_eq[j, off[j]:off[j + 1]] = 1.0
+    A_ub = inst.demand[b].astype(np.float64).T
+    ub = [(0.0, 0.0) if (inst.feasible is not None and inst.feasible[b, e] == 0) else (0.0, None)
+          for e in range(nnz)]
+    res = linprog(c, A_ub=A_ub, b_ub=inst.capacity[b], A_eq=A_eq, b_eq=np.ones(N), bounds=ub,
+                  method="highs")
+    assert res.status in (0, 2), res.message
+    return float("nan") if res.status == 2 else -float(res.fun)
+
+
+def exact_score(inst, b, e, lam) -> Fraction:
+    s = Fraction(float(inst.utility[b, e]))
+    for r in range(inst.R):
+        s -= Fraction(float(lam[r])) * Fraction(float(inst.demand[b, e, r]))
+    return s

@@ -1,0 +1,70 @@
+"""Run a compact battery of oracle pins against one oracle library build.
+
+Usage: python -m tests._pin_battery <path-to-liboracle.so>
+Exit status 0 when every pin passes, 1 when any fails.  Used to show that
+plausible mistakes planted in a copy of the oracle are caught."""
+import math
+import sys
+import traceback
+from fractions import Fraction
+
+import numpy as np
+
+import oracle
+import workloads
+from tests._helpers import exact_score, golden_instance, lp_optimum, read_golden
+
+
+def battery(L) -> None:
+    # hand-derived traces (Sec. 3.2.2 argmax, Eq. 8 update)
+    for name in ("hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt"):
+        g = read_golden(name)
+        res = oracle.Oracle(golden_instance(g), L).solve(trace_choice=True)
+        for i, row in enumerate(g["trace"]):
+            assert list(res["tr_choice"][i, 0]) == [int(x) for x in row[2]]
+            assert np.array_equal(res["tr_U"][i, 0], np.array(row[3]))
+            assert np.array_equal(res["tr_lam"][i, 0], np.array(row[4]))
+            assert res["tr_dual"][i, 0] == row[5][0]
+        assert list(res["choice"][0]) == [int(x) for x in g["final_choice"]]
+        for x in res["tr_lam"].ravel():
+            assert math.copysign(1.0, x) > 0
+    # step sizes
+    assert oracle.eta(1, 0.01, 1, L) == 0.01 and oracle.eta(1, 1.0, 4, L) == 0.5
+    assert oracle.eta(0, 0.3, 7, L) == 0.3
+    # exact sums against math.fsum
+    rng = np.random.default_rng(5)
+    for _ in range(10):
+        v = (rng.random(500) * np.exp2(rng.integers(-140, 120, 500))).astype(np.float32)
+        assert oracle.exact_sum_f32(v, L) == math.fsum(float(x) for x in v)
+    assert oracle.exact_sum_f32(np.array([2.0 ** 53, 1.0], np.float32), L) == 2.0 ** 53
+    assert oracle.exact_sum_f32(np.array([2.0 ** 53, 2.0, 1.0], np.float32), L) == 2.0 ** 53 + 4
+    # exact per-job optimality and LP weak duality on random instances
+    for seed in (3, 4):
+        inst = workloads.random_small(seed, 6, 5, 3, iters=40, eta0=0.1)
+        res = oracle.Oracle(inst, L).solve(trace_choice=True)
+        lams = np.concatenate([inst.lam0, res["tr_lam"][:-1, 0]], axis=0)
+        LP = lp_optimum(inst)
+        off = inst.offsets
+        for t in (0, 3, 39):
+            assert res["tr_dual"][t, 0] >= LP - 1e-7
+            for j in range(inst.N):
+                sc = [exact_score(inst, 0, e, lams[t]) for e in range(off[j], off[j + 1])]
+                c = int(res["tr_choice"][t, 0, j])
+                assert sc[c] == max(sc) and c == sc.index(max(sc))
+            U = res["tr_U"][t, 0]
+            for r in range(inst.R):
+                vals = [float(inst.demand[0, off[j] + res["tr_choice"][t, 0, j], r]) for j in range(inst.N)]
+                assert U[r] == math.fsum(vals)
+
+
+def main(path: str) -> int:
+    try:
+        battery(oracle.bind(path))
+    except Exception:                       # any failed pin
+        traceback.print_exc(limit=2)
+        return 1
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1]))

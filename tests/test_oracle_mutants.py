@@ -1,0 +1,64 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and check
+that the pin battery catches every one of them, while the unmodified oracle
+passes.  Each mutant is compiled to a temporary library and exercised in a
+child process so that a crashing mutant cannot take the test run down."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "esp_oracle.c")
+
+MUTANTS = {
+    "rent_drops_a_term": ("for (r = 1; r < p->R; r++) rent", "for (r = 2; r < p->R; r++) rent"),
+    "rent_wrong_price": ("rent = rent + (double)d[r] * lam[r];", "rent = rent + (double)d[r] * lam[0];"),
+    "score_sign": ("return (double)util_of(p, b)[e] - rent;", "return (double)util_of(p, b)[e] + rent;"),
+    "ties_to_highest": ("if (best_k < 0 || s > best)", "if (best_k < 0 || s >= best)"),
+    "update_sign": ("double g = U[r] - C[r];", "double g = C[r] - U[r];"),
+    "no_projection": ("lam[r] = (x > 0.0) ? x : 0.0;", "lam[r] = x;"),
+    "negative_zero": ("lam[r] = (x > 0.0) ? x : 0.0;", "lam[r] = (x > 0.0) ? x : -0.0;"),
+    "t_zero_based": ("return eta0 / sqrt((double)t);", "return eta0 / sqrt((double)(t + 1));"),
+    "rule_swapped": ("if (rule == ORC_STEP_INV_SQRT)", "if (rule != ORC_STEP_INV_SQRT)"),
+    "demand_transposed": ("acc_add_f32(&a, d[(p->offsets[j] + choice[j]) * p->R + r]);",
+                          "acc_add_f32(&a, d[r * p->nnz + p->offsets[j] + choice[j]]);"),
+    "demand_first_config": ("acc_add_f32(&a, d[(p->offsets[j] + choice[j]) * p->R + r]);",
+                            "acc_add_f32(&a, d[(p->offsets[j]) * p->R + r]);"),
+    "round_half_up": ("if (guard && (sticky || (m & 1u))) m += 1;", "if (guard) m += 1;"),
+    "truncating_sum": ("if (guard && (sticky || (m & 1u))) m += 1;", ";"),
+    "dual_drops_capacity": ("v = v + lam[r] * p->capacity[(int64_t)b * p->R + r];", ";"),
+    "select_skips_last": ("for (e = lo; e < hi; e++) {", "for (e = lo; e + 1 < hi; e++) {"),
+}
+
+
+def _build(tmp_path, name, text):
+    src = tmp_path / f"{name}.c"
+    src.write_text(text)
+    lib = tmp_path / f"lib{name}.so"
+    subprocess.run(["gcc", *oracle.CFLAGS, "-I", os.path.dirname(SRC), "-o", str(lib), str(src), "-lm"],
+                   check=True)
+    return str(lib)
+
+
+def _battery(lib):
+    return subprocess.run([sys.executable, "-m", "tests._pin_battery", lib], cwd=ROOT,
+                          capture_output=True, text=True, timeout=300)
+
+
+def test_unmodified_oracle_passes_battery(tmp_path):
+    lib = _build(tmp_path, "orig", open(SRC).read())
+    r = _battery(lib)
+    assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    text = open(SRC).read()
+    assert text.count(old) == 1, f"mutation site for {name} not unique"
+    lib = _build(tmp_path, name, text.replace(old, new))
+    r = _battery(lib)
+    assert r.returncode != 0, f"mutant {name} survived the pin battery"
