@@ -1,0 +1,169 @@
+"""Benchmark of the ESP hot path on one MI355X.
+
+A step is one esp_solve of the named workload: T price iterations (score ->
+select -> exact demand -> Eq. 8 update, one fused kernel launch each) plus the
+re-selection at the final prices, with the table resident in HBM.
+
+Prints one JSON line:
+  value        job-configurations scored per second (whole job)
+  roofline     the fused kernel's algorithmic bytes per launch (the table:
+               (1 + R) * 4 bytes per job-configuration) over its average launch
+               duration, against the 8 TB/s HBM peak
+  cpu_baseline the CPU oracle (single-threaded C) on a bounded sample of the
+               same workload, in the same unit
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="large", choices=["tiny", "small", "large", "ragged", "batched"])
+    ap.add_argument("--iters", type=int, default=0, help="override T (0 = the workload's own)")
+    ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_large.json"),
+                    help="HBM bytes per launch measured with rocprofv3 counters, if present")
+    return ap.parse_args()
+
+
+def _cpu_baseline(inst, budget_s: float) -> dict:
+    import numpy as np
+
+    import oracle
+
+    o = oracle.Oracle(inst)
+    lam = np.array(inst.lam0[0], dtype=np.float64)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        _, _, lam = o.step(0, lam, n + 1)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= inst.iters:
+            break
+    per_iter = el / n
+    return {
+        "value": inst.nnz / per_iter,
+        "unit": "job-configs/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{inst.name}: first {n} price iterations of cluster 0 from lambda^1 = 0 "
+                  f"({el:.1f} s, single-threaded C oracle, fp64)",
+        "iters_per_s": 1.0 / per_iter,
+    }
+
+
+def main() -> int:
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the path shards over jobs but no multi-GPU code is built", file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    import paper_2608_07971_amd as esp
+    import workloads
+
+    t_gen = time.perf_counter()
+    kw = {}
+    inst = workloads.make(args.config, **kw)
+    T = args.iters or inst.iters
+    print(f"[bench] {args.config}: B={inst.B} N={inst.N} R={inst.R} nnz={inst.nnz} T={T} "
+          f"(generated in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+    solver = esp.Solver(inst, "cuda:0", blocks_per_cluster=args.blocks)
+    stream = torch.cuda.Stream()
+    lam0 = solver.prices(inst.lam0)
+    lam = lam0.clone()
+    torch.cuda.synchronize()
+
+    def step():
+        lam.copy_(lam0)
+        solver.solve(lam, T, stream=stream)
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step()
+    torch.cuda.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(args.steps):
+            step()
+        ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = ev0.elapsed_time(ev1)
+    assert solver.device_status() == 0
+    ms_per_step = ms_total / args.steps
+    sec = ms_total / 1e3
+    configs = inst.B * inst.nnz
+    launches = (T + 1) * args.steps                  # T fused iterations + the final re-selection
+    bytes_per_launch = configs * (1 + inst.R) * 4
+    avg_launch_s = sec / launches
+    achieved = bytes_per_launch / avg_launch_s / 1e9
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            tj = json.load(open(args.traffic_json))
+            if tj.get("config") == args.config and tj.get("kernel_source_sha") == _kernel_sha():
+                traffic = tj.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    out = {
+        "metric": "job-configs scored/sec and price iterations/sec at 262k x 64 x 8; % HBM peak",
+        "value": configs * T * args.steps / sec,
+        "unit": "job-configs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": f"{args.config}: {inst.B} x {inst.N} jobs x "
+                               f"{inst.dense_k or 'CSR'} configs x {inst.R} resources, T={T}, fp32 table",
+                   "clusters": inst.B, "jobs": inst.N, "configs_per_job": inst.dense_k,
+                   "resources": inst.R, "iterations": T, "seed": inst.seed},
+        "iters_per_s": T * args.steps / sec,
+        "pct_hbm_peak": 100.0 * achieved / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "k_dense (fused score/select/demand/update)",
+                     "bytes_per_launch": bytes_per_launch, "avg_launch_us": avg_launch_s * 1e6},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = _cpu_baseline(inst, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    solver.close()
+    return 0
+
+
+def _kernel_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("esp_kernels.hip", "esp_internal.hpp"):
+        h.update(open(os.path.join(ROOT, "paper_2608_07971_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    sys.exit(main())

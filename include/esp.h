@@ -1,0 +1,188 @@
+/*
+ * esp.h -- C-ABI of the MI355X (gfx950) Elastic Shadow Pricing library.
+ *
+ * Elastic Shadow Pricing (paper Sec. 3.2) relaxes the per-resource capacity
+ * constraint (Eq. 3) of the job-configuration integer program (Eq. 1-5) with
+ * prices lambda_r >= 0 (Eq. 6).  For fixed prices every job j independently
+ * takes the configuration maximising u_jk - sum_r lambda_r d_jkr (Sec. 3.2.2);
+ * the prices then take the projected subgradient step of Eq. 8,
+ *     lambda_r <- max(0, lambda_r + eta_t (U_r - C_r)),  U_r = sum_j d_{j,c_j,r},
+ * with eta_t = eta0 (fixed) or eta0 / sqrt(t), and the loop repeats
+ * (Sec. 3.2.3; Alg. 1 "EspTatonnement" followed by a re-selection at the
+ * final prices).
+ *
+ * Conventions for every entry point:
+ *   - Every function returns an esp_status; nothing aborts or throws.
+ *   - "host" pointers are read during the call only; "device" pointers are
+ *     caller-owned device memory (any hipMalloc'ed or torch-allocated buffer)
+ *     that must stay valid until the work queued on the stream has finished.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls other than
+ *     esp_create, esp_device_status and esp_destroy only enqueue work: they
+ *     return before the GPU has run it.
+ *   - A context is not thread-safe; distinct contexts are independent.
+ *   - Arithmetic: scores in binary64 in a fixed order without fused
+ *     multiply-add: rent = d_0*l_0, rent = rent + d_r*l_r (r = 1..R-1),
+ *     s = u - rent, with the fp32 table values widened exactly.  The choice
+ *     is the lowest configuration index among equal best scores.  U_r is the
+ *     exact sum of the chosen fp32 demands rounded once to binary64
+ *     (round-to-nearest-even), so results do not depend on launch geometry.
+ *     Step sizes are computed on the host with IEEE division and square root.
+ *   - Errors found by the GPU (bad prices, bad choice indices) are recorded
+ *     in the context and reported by esp_device_status.
+ */
+#ifndef ESP_H
+#define ESP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ESP_OK = 0,
+    ESP_ERR_INVALID_ARG = 1,      /* NULL where required, bad enum, bad scalar */
+    ESP_ERR_SHAPE = 2,            /* sizes or CSR offsets inconsistent or out of range */
+    ESP_ERR_NONFINITE = 3,        /* NaN or +-Inf in utility, demand, capacity, eta0 or prices */
+    ESP_ERR_NEGATIVE_DEMAND = 4,  /* a demand entry below zero (Eq. 3 resources are >= 0) */
+    ESP_ERR_EMPTY_FAMILY = 5,     /* a job with no allowed configuration (Eq. 2 unsatisfiable) */
+    ESP_ERR_WORKSPACE = 6,        /* workspace NULL, not 256-byte aligned, or too small */
+    ESP_ERR_RANGE = 7,            /* magnitudes beyond what exact accumulation / fp64 can hold */
+    ESP_ERR_DEVICE = 8,           /* a HIP runtime call failed */
+    ESP_ERR_STATE = 9             /* NULL or destroyed context */
+} esp_status;
+
+/* Step rules of Eq. 8. */
+enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
+
+/* Opaque context: packed table + launch plan, created by esp_create. */
+typedef struct esp_ctx esp_ctx;
+
+/*
+ * The logical problem (Sec. 3.2.1): B independent clusters that share one
+ * job/family layout.  Entry e of the job x configuration table belongs to
+ * job j when offsets[j] <= e < offsets[j+1]; its configuration index within
+ * the family is k = e - offsets[j].  All pointers are HOST pointers read
+ * during esp_workspace_size / esp_create only.
+ */
+typedef struct {
+    int32_t num_clusters;            /* B >= 1 */
+    int32_t num_jobs;                /* N >= 1 jobs per cluster */
+    int32_t num_resources;           /* R in [1, 8] */
+    int32_t configs_per_job;         /* dense layout: K in [1, 256]; ignored when family_offsets != NULL */
+    const int64_t *family_offsets;   /* CSR [N+1], offsets[0] = 0, strictly increasing, family sizes
+                                        in [1, 256]; NULL selects the dense layout offsets[j] = j*K */
+    const float *utility;            /* [B][nnz]: u_jk, the value maximised (w_j T_j(c) of Eq. 1/6, or
+                                        T_j(c)/T_j(c_max) - Gamma_j(c) for the Eq. 7 form); finite */
+    const float *demand;             /* [B][nnz][R]: R_j(c)[r] of Eq. 3; finite and >= 0 */
+    const double *capacity;          /* [B][R]: C_r (or C_eff of Eq. 12); finite, |C_r| <= 2^200 */
+    const uint8_t *feasible;         /* optional [B][nnz]: 0 marks a configuration that violates the
+                                        performance floor of Eq. 4 (never selected); NULL = all allowed */
+} esp_problem;
+
+typedef struct {
+    int32_t rule;                    /* ESP_STEP_CONST or ESP_STEP_INV_SQRT */
+    const double *eta0;              /* host [B]: finite, 0 < eta0 <= 2^100 */
+} esp_step_rule;
+
+typedef struct {
+    int32_t blocks_per_cluster;      /* 0 = chosen by the library from the problem size */
+    int32_t reserved[7];             /* must be zero */
+} esp_options;
+
+/* Optional per-iteration record of esp_solve (device pointers, iteration-major;
+ * row i describes iteration t = t_start + i).  Any field may be NULL. */
+typedef struct {
+    double *prices;                  /* [T][B][R]: lambda^{t+1} after the update of iteration t */
+    double *demand;                  /* [T][B][R]: U^t at the selection made at lambda^t */
+    int32_t *choice;                 /* [T][B][N]: c^t */
+} esp_trace;
+
+/*
+ * esp_workspace_size: device workspace bytes esp_create needs for `problem`
+ * (only its shapes and offsets are read).  `options` may be NULL.
+ * Errors: ESP_ERR_INVALID_ARG (NULL problem/bytes, reserved options nonzero),
+ * ESP_ERR_SHAPE.
+ */
+esp_status esp_workspace_size(const esp_problem *problem, const esp_options *options, size_t *bytes);
+
+/*
+ * esp_create: validate the problem, pack the table into the structure-of-
+ * arrays device image inside `workspace` and return a context.  The workspace
+ * is caller-owned device memory of at least esp_workspace_size bytes,
+ * 256-byte aligned, which must outlive the context; its contents are
+ * overwritten.  Host arrays may be freed when the call returns (it waits for
+ * its own copies on `stream`).
+ * Errors: ESP_ERR_INVALID_ARG, ESP_ERR_SHAPE, ESP_ERR_NONFINITE,
+ * ESP_ERR_NEGATIVE_DEMAND, ESP_ERR_EMPTY_FAMILY, ESP_ERR_WORKSPACE,
+ * ESP_ERR_RANGE (a demand column whose exact sum does not fit the 128-bit
+ * accumulator: its nonzero values span too many binary orders of magnitude),
+ * ESP_ERR_DEVICE.  On error *out is set to NULL.
+ */
+esp_status esp_create(const esp_problem *problem, const esp_step_rule *step, const esp_options *options,
+                      void *workspace, size_t workspace_bytes, void *stream, esp_ctx **out);
+
+/*
+ * esp_score_select (Sec. 3.2.2): for prices `prices` (device [B][R], finite,
+ * >= 0) write every job's best configuration index to `choice` (device
+ * [B][N] int32).  Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ */
+esp_status esp_score_select(esp_ctx *ctx, const double *prices, int32_t *choice, void *stream);
+
+/*
+ * esp_reduce_demand (Sec. 3.2.3, U_r under Eq. 8): demand (device [B][R]) =
+ * exact per-resource sum of the demands of the configurations in `choice`
+ * (device [B][N]).  An index outside a job's family makes that cluster's
+ * demand NaN and is reported by esp_device_status.
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ */
+esp_status esp_reduce_demand(esp_ctx *ctx, const int32_t *choice, double *demand, void *stream);
+
+/*
+ * esp_update_prices (Eq. 8): prices (device [B][R], in lambda^t, out
+ * lambda^{t+1}) <- max(0, lambda + eta_t (demand - C)); t >= 1 selects
+ * eta_t.  Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ */
+esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, double *prices, void *stream);
+
+/*
+ * esp_solve: `iters` iterations t = t_start .. t_start+iters-1 of
+ * select -> demand -> update, one fused kernel per iteration (the update runs
+ * in the last workgroup of each cluster), then a re-selection at the final
+ * prices (Alg. 1).
+ *   prices      device [B][R], in lambda^{t_start} (finite, >= 0), out the final prices
+ *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
+ *   tol         0 = run all T iterations; > 0 = a cluster stops after the first
+ *               update with |lambda^{t+1}_r - lambda^t_r| <= tol * max(1, lambda^t_r)
+ *               for every r (its later iterations do nothing)
+ *   choice      device [B][N] or NULL: selection at the final prices
+ *   demand      device [B][R] or NULL: U at that selection
+ *   trace       NULL or per-iteration records (see esp_trace)
+ *   iters_done  device [B] int32 or NULL: updates made per cluster
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ */
+esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_start, double tol,
+                     int32_t *choice, double *demand, const esp_trace *trace, int32_t *iters_done,
+                     void *stream);
+
+/*
+ * esp_device_status: wait for `stream`, then return (and clear) the first
+ * error the GPU recorded since the last call: ESP_ERR_NONFINITE or
+ * ESP_ERR_INVALID_ARG for prices that were NaN, infinite or negative (the
+ * affected calls left prices and outputs unchanged), ESP_ERR_INVALID_ARG for
+ * a choice index outside its family; ESP_OK otherwise.
+ */
+esp_status esp_device_status(esp_ctx *ctx, void *stream);
+
+/* esp_destroy: free the host-side context (the workspace stays the caller's).
+ * Waits for nothing: the caller must not destroy a context with work in flight. */
+esp_status esp_destroy(esp_ctx *ctx);
+
+/* Static, NUL-terminated description of a status code. */
+const char *esp_status_string(esp_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ESP_H */

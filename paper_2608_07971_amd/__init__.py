@@ -1,0 +1,271 @@
+"""Python binding of the MI355X Elastic Shadow Pricing library (libesp.so).
+
+The functions below carry the names of the C-ABI in include/esp.h and only
+marshal arguments: every step of the method runs in the HIP kernels of
+csrc/.  PyTorch provides device memory (the workspace and per-call tensors)
+and streams.  There is no CPU fallback: importing the binding without a built
+libesp.so raises, and so does calling it without a GPU.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+import torch  # loaded first so libesp.so binds to the HIP runtime torch uses
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libesp.so")
+
+ESP_OK = 0
+ESP_ERR_INVALID_ARG = 1
+ESP_ERR_SHAPE = 2
+ESP_ERR_NONFINITE = 3
+ESP_ERR_NEGATIVE_DEMAND = 4
+ESP_ERR_EMPTY_FAMILY = 5
+ESP_ERR_WORKSPACE = 6
+ESP_ERR_RANGE = 7
+ESP_ERR_DEVICE = 8
+ESP_ERR_STATE = 9
+
+ESP_STEP_CONST = 0
+ESP_STEP_INV_SQRT = 1
+
+
+class EspError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} (status {code})")
+
+
+class esp_problem(C.Structure):
+    _fields_ = [
+        ("num_clusters", C.c_int32), ("num_jobs", C.c_int32), ("num_resources", C.c_int32),
+        ("configs_per_job", C.c_int32), ("family_offsets", C.c_void_p), ("utility", C.c_void_p),
+        ("demand", C.c_void_p), ("capacity", C.c_void_p), ("feasible", C.c_void_p),
+    ]
+
+
+class esp_step_rule(C.Structure):
+    _fields_ = [("rule", C.c_int32), ("eta0", C.c_void_p)]
+
+
+class esp_options(C.Structure):
+    _fields_ = [("blocks_per_cluster", C.c_int32), ("reserved", C.c_int32 * 7)]
+
+
+class esp_trace(C.Structure):
+    _fields_ = [("prices", C.c_void_p), ("demand", C.c_void_p), ("choice", C.c_void_p)]
+
+
+_lib = None
+
+# Every entry point of include/esp.h with its ctypes signature.
+_SIGS = {
+    "esp_workspace_size": ([C.c_void_p, C.c_void_p, C.POINTER(C.c_size_t)], C.c_int),
+    "esp_create": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p,
+                    C.POINTER(C.c_void_p)], C.c_int),
+    "esp_score_select": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_reduce_demand": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_update_prices": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_solve": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_void_p,
+                   C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
+    "esp_destroy": ([C.c_void_p], C.c_int),
+    "esp_status_string": ([C.c_int], C.c_char_p),
+}
+
+
+def lib():
+    """Load libesp.so (raises when it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(there is no CPU fallback)")
+        L = C.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().esp_status_string(code).decode()
+
+
+def _check(code: int, where: str) -> None:
+    if code != ESP_OK:
+        raise EspError(code, where)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        if not t.is_cuda:
+            raise ValueError("device tensor expected")
+        if not t.is_contiguous():
+            raise ValueError("contiguous tensor expected")
+        return t.data_ptr()
+    return int(t)
+
+
+# ---------------------------------------------------------------------------
+# C-ABI entry points (same names as include/esp.h)
+# ---------------------------------------------------------------------------
+
+class Problem:
+    """Host arrays of an esp_problem kept alive for the duration of a call."""
+
+    def __init__(self, offsets, utility, demand, capacity, feasible=None, dense_k: Optional[int] = None):
+        self.utility = np.ascontiguousarray(utility, dtype=np.float32)
+        self.demand = np.ascontiguousarray(demand, dtype=np.float32)
+        self.capacity = np.ascontiguousarray(capacity, dtype=np.float64)
+        self.feasible = None if feasible is None else np.ascontiguousarray(feasible, dtype=np.uint8)
+        self.offsets = None if dense_k else np.ascontiguousarray(offsets, dtype=np.int64)
+        B = self.utility.shape[0]
+        R = self.demand.shape[-1]
+        N = (self.utility.shape[1] // dense_k) if dense_k else self.offsets.size - 1
+        self.B, self.N, self.R = B, N, R
+        self.c = esp_problem(B, N, R, int(dense_k or 0),
+                             None if self.offsets is None else self.offsets.ctypes.data,
+                             self.utility.ctypes.data, self.demand.ctypes.data, self.capacity.ctypes.data,
+                             None if self.feasible is None else self.feasible.ctypes.data)
+
+    @classmethod
+    def from_instance(cls, inst) -> "Problem":
+        return cls(inst.offsets, inst.utility, inst.demand, inst.capacity, inst.feasible,
+                   dense_k=getattr(inst, "dense_k", None))
+
+
+def esp_workspace_size(problem: Problem, options: Optional[esp_options] = None) -> int:
+    n = C.c_size_t(0)
+    _check(lib().esp_workspace_size(C.addressof(problem.c), None if options is None else C.addressof(options),
+                                    C.byref(n)), "esp_workspace_size")
+    return int(n.value)
+
+
+def esp_create(problem: Problem, rule: int, eta0, workspace, options: Optional[esp_options] = None,
+               stream=None) -> int:
+    e0 = np.ascontiguousarray(eta0, dtype=np.float64)
+    step = esp_step_rule(int(rule), e0.ctypes.data)
+    out = C.c_void_p(None)
+    _check(lib().esp_create(C.addressof(problem.c), C.addressof(step),
+                            None if options is None else C.addressof(options), _ptr(workspace),
+                            workspace.numel() * workspace.element_size(), _stream(stream), C.byref(out)),
+           "esp_create")
+    return int(out.value)
+
+
+def esp_score_select(ctx: int, prices, choice, stream=None) -> None:
+    _check(lib().esp_score_select(ctx, _ptr(prices), _ptr(choice), _stream(stream)), "esp_score_select")
+
+
+def esp_reduce_demand(ctx: int, choice, demand, stream=None) -> None:
+    _check(lib().esp_reduce_demand(ctx, _ptr(choice), _ptr(demand), _stream(stream)), "esp_reduce_demand")
+
+
+def esp_update_prices(ctx: int, demand, t: int, prices, stream=None) -> None:
+    _check(lib().esp_update_prices(ctx, _ptr(demand), int(t), _ptr(prices), _stream(stream)),
+           "esp_update_prices")
+
+
+def esp_solve(ctx: int, prices, iters: int, t_start: int = 1, tol: float = 0.0, choice=None, demand=None,
+              trace: Optional[esp_trace] = None, iters_done=None, stream=None) -> None:
+    _check(lib().esp_solve(ctx, _ptr(prices), int(iters), int(t_start), float(tol), _ptr(choice), _ptr(demand),
+                           None if trace is None else C.addressof(trace), _ptr(iters_done), _stream(stream)),
+           "esp_solve")
+
+
+def esp_device_status(ctx: int, stream=None) -> int:
+    return int(lib().esp_device_status(ctx, _stream(stream)))
+
+
+def esp_destroy(ctx: int) -> None:
+    _check(lib().esp_destroy(ctx), "esp_destroy")
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrapper: owns the workspace tensor and the context
+# ---------------------------------------------------------------------------
+
+class Solver:
+    """A packed problem on one GPU.  `inst` is any object with the fields of a
+    logical problem (offsets, utility, demand, capacity, feasible, eta0, rule,
+    dense_k)."""
+
+    def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, stream=None):
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU: the ESP library has no CPU path")
+        self.device = torch.device(device)
+        self.problem = Problem.from_instance(inst)
+        self.B, self.N, self.R = self.problem.B, self.problem.N, self.problem.R
+        self.options = esp_options(int(blocks_per_cluster))
+        nbytes = esp_workspace_size(self.problem, self.options)
+        self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        with torch.cuda.device(self.device):
+            self.ctx = esp_create(self.problem, int(inst.rule), inst.eta0, self.workspace, self.options, stream)
+        self.problem = None            # host arrays are no longer needed
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            esp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def prices(self, lam) -> torch.Tensor:
+        return torch.as_tensor(np.asarray(lam, dtype=np.float64).reshape(self.B, self.R),
+                               device=self.device).contiguous()
+
+    def score_select(self, prices: torch.Tensor, stream=None) -> torch.Tensor:
+        ch = torch.empty((self.B, self.N), dtype=torch.int32, device=self.device)
+        esp_score_select(self.ctx, prices, ch, stream)
+        return ch
+
+    def reduce_demand(self, choice: torch.Tensor, stream=None) -> torch.Tensor:
+        U = torch.empty((self.B, self.R), dtype=torch.float64, device=self.device)
+        esp_reduce_demand(self.ctx, choice, U, stream)
+        return U
+
+    def update_prices(self, demand: torch.Tensor, t: int, prices: torch.Tensor, stream=None) -> None:
+        esp_update_prices(self.ctx, demand, t, prices, stream)
+
+    def solve(self, prices: torch.Tensor, iters: int, t_start: int = 1, tol: float = 0.0, trace: bool = False,
+              trace_choice: bool = False, stream=None) -> dict:
+        """Run `iters` iterations in place on `prices`; returns device tensors."""
+        out = {
+            "choice": torch.empty((self.B, self.N), dtype=torch.int32, device=self.device),
+            "U": torch.empty((self.B, self.R), dtype=torch.float64, device=self.device),
+            "iters_done": torch.empty(self.B, dtype=torch.int32, device=self.device),
+        }
+        tr = None
+        if trace or trace_choice:
+            T = max(int(iters), 1)
+            if trace:
+                out["tr_lam"] = torch.full((T, self.B, self.R), float("nan"), dtype=torch.float64,
+                                           device=self.device)
+                out["tr_U"] = torch.full((T, self.B, self.R), float("nan"), dtype=torch.float64, device=self.device)
+            if trace_choice:
+                out["tr_choice"] = torch.full((T, self.B, self.N), -1, dtype=torch.int32, device=self.device)
+            tr = esp_trace(_ptr(out.get("tr_lam")), _ptr(out.get("tr_U")), _ptr(out.get("tr_choice")))
+        esp_solve(self.ctx, prices, iters, t_start, tol, out["choice"], out["U"], tr, out["iters_done"], stream)
+        out["lam"] = prices
+        return out
+
+    def device_status(self, stream=None) -> int:
+        return esp_device_status(self.ctx, stream)

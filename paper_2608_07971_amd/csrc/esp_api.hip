@@ -1,0 +1,550 @@
+// Host side of the Elastic Shadow Pricing C-ABI (include/esp.h): argument
+// validation, the packer that lays the job x configuration table out as
+// structure-of-arrays tiles in the caller's device workspace, and the drivers
+// that enqueue the kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/esp.h"
+#include "esp_internal.hpp"
+
+#pragma clang fp contract(off)
+
+using namespace esp;
+
+namespace {
+
+constexpr uint32_t kMagic = 0x45535031u;   // "ESP1"
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Launch plan and workspace layout derived from the problem's shapes.
+struct Plan {
+    int B = 0, N = 0, R = 0;
+    int K = 0;          // dense family size handled by the dense kernel, else 0
+    int lpj = 0;        // lanes per job of the dense kernel
+    bool csr = false;
+    int64_t nnz = 0;
+    int tiles = 0;      // per cluster
+    size_t col_len = 0; // floats per column
+    int nblk = 0;       // workgroups per cluster
+    // workspace offsets (bytes)
+    size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
+           o_tick = 0, o_flags = 0, o_iters = 0, o_status = 0, total = 0;
+};
+
+bool dense_fast_k(int K) { return K == 4 || K == 8 || K == 16 || K == 32 || K == 64; }
+
+// Family sizes of the problem (dense or CSR) and validation of the offsets.
+esp_status family_layout(const esp_problem *p, std::vector<int64_t> *sizes_out, int *uniform_k) {
+    const int N = p->num_jobs;
+    *uniform_k = 0;
+    if (p->family_offsets == nullptr) {
+        if (p->configs_per_job < 1 || p->configs_per_job > kMaxFamily) return ESP_ERR_SHAPE;
+        *uniform_k = p->configs_per_job;
+        return ESP_OK;
+    }
+    const int64_t *off = p->family_offsets;
+    if (off[0] != 0) return ESP_ERR_SHAPE;
+    int64_t k0 = -1;
+    bool uniform = true;
+    for (int j = 0; j < N; ++j) {
+        const int64_t k = off[j + 1] - off[j];
+        if (k < 1 || k > kMaxFamily) return ESP_ERR_SHAPE;
+        if (k0 < 0) k0 = k;
+        uniform = uniform && (k == k0);
+    }
+    if (uniform) *uniform_k = static_cast<int>(k0);
+    if (sizes_out) {
+        sizes_out->resize(N);
+        for (int j = 0; j < N; ++j) (*sizes_out)[j] = off[j + 1] - off[j];
+    }
+    return ESP_OK;
+}
+
+esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
+    if (p == nullptr) return ESP_ERR_INVALID_ARG;
+    if (opt) {
+        if (opt->blocks_per_cluster < 0) return ESP_ERR_INVALID_ARG;
+        for (int i = 0; i < 7; ++i)
+            if (opt->reserved[i] != 0) return ESP_ERR_INVALID_ARG;
+    }
+    if (p->num_clusters < 1 || p->num_jobs < 1 || p->num_resources < 1 || p->num_resources > kMaxR)
+        return ESP_ERR_SHAPE;
+    const int64_t BN = static_cast<int64_t>(p->num_clusters) * p->num_jobs;
+    if (BN > INT32_MAX) return ESP_ERR_SHAPE;
+    int uk = 0;
+    esp_status st = family_layout(p, nullptr, &uk);
+    if (st != ESP_OK) return st;
+    pl->B = p->num_clusters;
+    pl->N = p->num_jobs;
+    pl->R = p->num_resources;
+    if (uk > 0 && dense_fast_k(uk)) {
+        pl->K = uk;
+        pl->lpj = uk / 4;
+        const int jpt = kWaveSize / pl->lpj;
+        pl->nnz = static_cast<int64_t>(pl->N) * uk;
+        pl->tiles = static_cast<int>((static_cast<int64_t>(pl->N) + jpt - 1) / jpt);
+    } else {
+        // CSR tiles: whole families packed greedily into 256-entry tiles.
+        const int N = pl->N;
+        int64_t tiles = 0, fill = kTileEntries, nnz = 0;
+        for (int j = 0; j < N; ++j) {
+            const int64_t k = p->family_offsets ? p->family_offsets[j + 1] - p->family_offsets[j]
+                                                : p->configs_per_job;
+            if (fill + k > kTileEntries) { ++tiles; fill = 0; }
+            fill += k;
+            nnz += k;
+        }
+        pl->csr = true;
+        pl->nnz = nnz;
+        if (tiles > INT32_MAX / 2) return ESP_ERR_SHAPE;
+        pl->tiles = static_cast<int>(tiles);
+    }
+    pl->col_len = static_cast<size_t>(pl->tiles) * kTileEntries;
+    if (pl->col_len >= (static_cast<size_t>(1) << 32)) return ESP_ERR_SHAPE;
+    // Workgroups: about 1024 in flight over the whole device, split across clusters.
+    const int max_useful = std::max(1, (pl->tiles + kBlockWaves - 1) / kBlockWaves);
+    int nblk = (opt && opt->blocks_per_cluster > 0) ? opt->blocks_per_cluster
+                                                     : std::max(1, (1024 + pl->B - 1) / pl->B);
+    pl->nblk = std::min(nblk, max_useful);
+    if (static_cast<int64_t>(pl->nblk) * pl->B > INT32_MAX) return ESP_ERR_SHAPE;
+
+    const size_t B = pl->B, R = pl->R;
+    size_t o = 0;
+    pl->o_table = o; o = align_up(o + B * (R + 1) * pl->col_len * sizeof(float));
+    pl->o_meta = o;  o = align_up(o + (pl->csr ? static_cast<size_t>(pl->tiles) * sizeof(TileMeta) : 0));
+    pl->o_jobs = o;  o = align_up(o + (pl->csr ? static_cast<size_t>(pl->N) * sizeof(JobSlot) : 0));
+    pl->o_shift = o; o = align_up(o + B * R * sizeof(int32_t));
+    pl->o_cap = o;   o = align_up(o + B * R * sizeof(double));
+    pl->o_eta = o;   o = align_up(o + B * kEtaChunk * sizeof(double));
+    pl->o_part = o;  o = align_up(o + B * pl->nblk * R * 2 * sizeof(uint64_t));
+    pl->o_tick = o;  o = align_up(o + B * sizeof(uint32_t));
+    pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
+    pl->o_iters = o; o = align_up(o + B * sizeof(int32_t));
+    pl->o_status = o; o = align_up(o + sizeof(int32_t));
+    pl->total = o;
+    return ESP_OK;
+}
+
+// Lowest set bit exponent and bit length of a positive finite float:
+// v = m * 2^x with m odd; top = exponent of the bit above the highest set bit.
+void float_bits(float v, int *low, int *top) {
+    uint32_t b;
+    std::memcpy(&b, &v, 4);
+    const uint32_t e = b >> 23;
+    const uint32_t m = (b & 0x7fffffu) | (e ? 0x800000u : 0u);
+    const int x = (e ? static_cast<int>(e) : 1) - 150;
+    *low = x + __builtin_ctz(m);
+    *top = x + (32 - __builtin_clz(m));
+}
+
+struct PinnedPair {
+    float *buf[2] = {nullptr, nullptr};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    bool pending[2] = {false, false};
+    size_t cap = 0;
+    ~PinnedPair() {
+        for (int i = 0; i < 2; ++i) {
+            if (ev[i]) { if (pending[i]) (void)hipEventSynchronize(ev[i]); (void)hipEventDestroy(ev[i]); }
+            if (buf[i]) (void)hipHostFree(buf[i]);
+        }
+    }
+};
+
+}  // namespace
+
+struct esp_ctx {
+    uint32_t magic = kMagic;
+    Plan pl;
+    int rule = 0;
+    std::vector<double> eta0;
+    char *ws = nullptr;
+    double *h_eta = nullptr;           // pinned staging for step sizes
+    hipEvent_t eta_ev = nullptr;
+    bool eta_pending = false;
+    KArgs base{};
+};
+
+namespace {
+
+esp_status check_ctx(const esp_ctx *c) {
+    return (c != nullptr && c->magic == kMagic) ? ESP_OK : ESP_ERR_STATE;
+}
+
+esp_status dev(hipError_t e) { return e == hipSuccess ? ESP_OK : ESP_ERR_DEVICE; }
+
+// Stage step sizes eta_t for t = t0 .. t0+n-1 (n <= kEtaChunk) into the
+// workspace table row-major [i][b].  IEEE division and square root on the host.
+esp_status stage_eta(esp_ctx *c, int64_t t0, int n, hipStream_t s) {
+    const int B = c->pl.B;
+    if (c->eta_pending) {
+        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
+        c->eta_pending = false;
+    }
+    for (int i = 0; i < n; ++i) {
+        const double t = static_cast<double>(t0 + i);
+        for (int b = 0; b < B; ++b)
+            c->h_eta[static_cast<size_t>(i) * B + b] =
+                (c->rule == ESP_STEP_INV_SQRT) ? c->eta0[b] / std::sqrt(t) : c->eta0[b];
+    }
+    double *d_eta = reinterpret_cast<double *>(c->ws + c->pl.o_eta);
+    if (hipMemcpyAsync(d_eta, c->h_eta, sizeof(double) * static_cast<size_t>(n) * B, hipMemcpyHostToDevice, s) !=
+        hipSuccess)
+        return ESP_ERR_DEVICE;
+    if (hipEventRecord(c->eta_ev, s) != hipSuccess) return ESP_ERR_DEVICE;
+    c->eta_pending = true;
+    return ESP_OK;
+}
+
+hipError_t launch_select(const esp_ctx *c, const KArgs &a, hipStream_t s) {
+    return c->pl.csr ? launch_csr(c->pl.R, a, c->pl.B, s) : launch_dense(c->pl.R, c->pl.lpj, a, c->pl.B, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *esp_status_string(esp_status st) {
+    switch (st) {
+        case ESP_OK: return "ok";
+        case ESP_ERR_INVALID_ARG: return "invalid argument";
+        case ESP_ERR_SHAPE: return "inconsistent or unsupported shape";
+        case ESP_ERR_NONFINITE: return "non-finite input value";
+        case ESP_ERR_NEGATIVE_DEMAND: return "negative demand";
+        case ESP_ERR_EMPTY_FAMILY: return "job with no allowed configuration";
+        case ESP_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case ESP_ERR_RANGE: return "value range not supported";
+        case ESP_ERR_DEVICE: return "HIP runtime error";
+        case ESP_ERR_STATE: return "invalid context";
+    }
+    return "unknown status";
+}
+
+esp_status esp_workspace_size(const esp_problem *problem, const esp_options *options, size_t *bytes) {
+    if (bytes == nullptr) return ESP_ERR_INVALID_ARG;
+    Plan pl;
+    esp_status st = make_plan(problem, options, &pl);
+    if (st != ESP_OK) return st;
+    *bytes = pl.total;
+    return ESP_OK;
+}
+
+esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp_options *options,
+                      void *workspace, size_t workspace_bytes, void *stream, esp_ctx **out) {
+    if (out == nullptr) return ESP_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (p == nullptr || step == nullptr || p->utility == nullptr || p->demand == nullptr ||
+        p->capacity == nullptr || step->eta0 == nullptr)
+        return ESP_ERR_INVALID_ARG;
+    if (step->rule != ESP_STEP_CONST && step->rule != ESP_STEP_INV_SQRT) return ESP_ERR_INVALID_ARG;
+    Plan pl;
+    esp_status st = make_plan(p, options, &pl);
+    if (st != ESP_OK) return st;
+    const int B = pl.B, N = pl.N, R = pl.R;
+    const int64_t nnz = pl.nnz;
+
+    // ---- validate values (host) ----
+    for (int b = 0; b < B; ++b) {
+        const double e0 = step->eta0[b];
+        if (!std::isfinite(e0)) return ESP_ERR_NONFINITE;
+        if (!(e0 > 0.0)) return ESP_ERR_INVALID_ARG;
+        if (e0 > 0x1p100) return ESP_ERR_RANGE;
+        for (int r = 0; r < R; ++r) {
+            const double cr = p->capacity[static_cast<size_t>(b) * R + r];
+            if (!std::isfinite(cr)) return ESP_ERR_NONFINITE;
+            if (std::fabs(cr) > 0x1p200) return ESP_ERR_RANGE;
+        }
+    }
+    std::vector<int64_t> off(static_cast<size_t>(N) + 1);
+    for (int j = 0; j <= N; ++j)
+        off[j] = p->family_offsets ? p->family_offsets[j] : static_cast<int64_t>(j) * p->configs_per_job;
+    const size_t BNNZ = static_cast<size_t>(B) * static_cast<size_t>(nnz);
+    for (size_t e = 0; e < BNNZ; ++e)
+        if (!std::isfinite(p->utility[e])) return ESP_ERR_NONFINITE;
+    for (size_t e = 0; e < BNNZ * R; ++e) {
+        const float v = p->demand[e];
+        if (!std::isfinite(v)) return ESP_ERR_NONFINITE;
+        if (v < 0.0f) return ESP_ERR_NEGATIVE_DEMAND;
+    }
+    if (p->feasible) {
+        for (int b = 0; b < B; ++b)
+            for (int j = 0; j < N; ++j) {
+                bool any = false;
+                for (int64_t e = off[j]; e < off[j + 1] && !any; ++e)
+                    any = p->feasible[static_cast<size_t>(b) * nnz + e] != 0;
+                if (!any) return ESP_ERR_EMPTY_FAMILY;
+            }
+    }
+    // Fixed-point window per (cluster, resource): lowest set bit over the
+    // column; the highest bit plus log2(N) must stay below 2^127.
+    std::vector<int32_t> shift(static_cast<size_t>(B) * R, 0);
+    int lgN = 0;
+    while ((static_cast<int64_t>(1) << lgN) < static_cast<int64_t>(N) + 1) ++lgN;
+    for (int b = 0; b < B; ++b)
+        for (int r = 0; r < R; ++r) {
+            int lo = INT32_MAX, hi = INT32_MIN;
+            const float *d = p->demand + static_cast<size_t>(b) * nnz * R + r;
+            for (int64_t e = 0; e < nnz; ++e) {
+                const float v = d[static_cast<size_t>(e) * R];
+                if (v == 0.0f) continue;
+                int l, t;
+                float_bits(v, &l, &t);
+                lo = std::min(lo, l);
+                hi = std::max(hi, t);
+            }
+            if (lo == INT32_MAX) { shift[static_cast<size_t>(b) * R + r] = 0; continue; }
+            if (hi - lo + lgN > 127) return ESP_ERR_RANGE;
+            shift[static_cast<size_t>(b) * R + r] = lo;
+        }
+
+    // ---- workspace ----
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0 || workspace_bytes < pl.total)
+        return ESP_ERR_WORKSPACE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    char *ws = static_cast<char *>(workspace);
+
+    esp_ctx *c = new (std::nothrow) esp_ctx();
+    if (c == nullptr) return ESP_ERR_DEVICE;
+    c->pl = pl;
+    c->rule = step->rule;
+    c->eta0.assign(step->eta0, step->eta0 + B);
+    c->ws = ws;
+    auto fail = [&](esp_status e) {
+        if (c->h_eta) (void)hipHostFree(c->h_eta);
+        if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
+        delete c;
+        return e;
+    };
+    if (hipHostMalloc(reinterpret_cast<void **>(&c->h_eta), sizeof(double) * B * kEtaChunk) != hipSuccess)
+        return fail(ESP_ERR_DEVICE);
+    if (hipEventCreateWithFlags(&c->eta_ev, hipEventDisableTiming) != hipSuccess) return fail(ESP_ERR_DEVICE);
+
+    // ---- pack the table: one column at a time through two pinned buffers ----
+    std::vector<TileMeta> meta;
+    std::vector<JobSlot> jobs;
+    std::vector<int64_t> slot_of(N);
+    if (pl.csr) {
+        meta.assign(pl.tiles, TileMeta{});
+        jobs.resize(N);
+        int64_t tile = -1, fill = kTileEntries;
+        for (int j = 0; j < N; ++j) {
+            const int64_t k = off[j + 1] - off[j];
+            if (fill + k > kTileEntries) {
+                ++tile;
+                fill = 0;
+                meta[tile].first_job = static_cast<uint32_t>(j);
+            }
+            meta[tile].head[fill / 32] |= 1u << (fill % 32);
+            slot_of[j] = tile * kTileEntries + fill;
+            jobs[j].slot = static_cast<uint32_t>(slot_of[j]);
+            jobs[j].size = static_cast<uint32_t>(k);
+            fill += k;
+        }
+    } else {
+        for (int j = 0; j < N; ++j) slot_of[j] = static_cast<int64_t>(j) * pl.K;
+    }
+    {
+        PinnedPair pp;
+        pp.cap = pl.col_len;
+        for (int i = 0; i < 2; ++i) {
+            if (hipHostMalloc(reinterpret_cast<void **>(&pp.buf[i]), sizeof(float) * pp.cap) != hipSuccess)
+                return fail(ESP_ERR_DEVICE);
+            if (hipEventCreateWithFlags(&pp.ev[i], hipEventDisableTiming) != hipSuccess) return fail(ESP_ERR_DEVICE);
+        }
+        const float neg_inf = -__builtin_inff();
+        const float pad_u = pl.csr ? neg_inf : 0.0f;
+        int which = 0;
+        for (int b = 0; b < B; ++b) {
+            for (int a = 0; a <= R; ++a) {
+                if (pp.pending[which]) {
+                    if (hipEventSynchronize(pp.ev[which]) != hipSuccess) return fail(ESP_ERR_DEVICE);
+                    pp.pending[which] = false;
+                }
+                float *h = pp.buf[which];
+                std::fill(h, h + pl.col_len, a == 0 ? pad_u : 0.0f);
+                const float *u = p->utility + static_cast<size_t>(b) * nnz;
+                const float *d = p->demand + static_cast<size_t>(b) * nnz * R + (a - 1);
+                const uint8_t *f = p->feasible ? p->feasible + static_cast<size_t>(b) * nnz : nullptr;
+                for (int j = 0; j < N; ++j) {
+                    const int64_t e0 = off[j], k = off[j + 1] - off[j];
+                    float *dst = h + slot_of[j];
+                    if (a == 0) {
+                        for (int64_t i = 0; i < k; ++i)
+                            dst[i] = (f && f[e0 + i] == 0) ? neg_inf : u[e0 + i];
+                    } else {
+                        for (int64_t i = 0; i < k; ++i) {
+                            const float v = d[static_cast<size_t>(e0 + i) * R];
+                            dst[i] = (v == 0.0f) ? 0.0f : v;     // -0.0 -> +0.0
+                        }
+                    }
+                }
+                float *dcol = reinterpret_cast<float *>(ws + pl.o_table) +
+                              (static_cast<size_t>(b) * (R + 1) + a) * pl.col_len;
+                if (hipMemcpyAsync(dcol, h, sizeof(float) * pl.col_len, hipMemcpyHostToDevice, s) != hipSuccess ||
+                    hipEventRecord(pp.ev[which], s) != hipSuccess)
+                    return fail(ESP_ERR_DEVICE);
+                pp.pending[which] = true;
+                which ^= 1;
+            }
+        }
+        std::vector<double> cap(p->capacity, p->capacity + static_cast<size_t>(B) * R);
+        bool ok = hipMemcpyAsync(ws + pl.o_shift, shift.data(), sizeof(int32_t) * shift.size(),
+                                 hipMemcpyHostToDevice, s) == hipSuccess &&
+                  hipMemcpyAsync(ws + pl.o_cap, cap.data(), sizeof(double) * cap.size(), hipMemcpyHostToDevice, s) ==
+                      hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_tick, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess;
+        if (ok && pl.csr)
+            ok = hipMemcpyAsync(ws + pl.o_meta, meta.data(), sizeof(TileMeta) * meta.size(), hipMemcpyHostToDevice,
+                                s) == hipSuccess &&
+                 hipMemcpyAsync(ws + pl.o_jobs, jobs.data(), sizeof(JobSlot) * jobs.size(), hipMemcpyHostToDevice,
+                                s) == hipSuccess;
+        if (!ok || hipStreamSynchronize(s) != hipSuccess) return fail(ESP_ERR_DEVICE);
+        pp.pending[0] = pp.pending[1] = false;
+    }
+
+    KArgs &k = c->base;
+    k.table = reinterpret_cast<const float *>(ws + pl.o_table);
+    k.cluster_stride = static_cast<size_t>(R + 1) * pl.col_len;
+    k.col_len = pl.col_len;
+    k.meta = pl.csr ? reinterpret_cast<const TileMeta *>(ws + pl.o_meta) : nullptr;
+    k.jobs = pl.csr ? reinterpret_cast<const JobSlot *>(ws + pl.o_jobs) : nullptr;
+    k.N = N;
+    k.K = pl.csr ? 0 : pl.K;
+    k.tiles = pl.tiles;
+    k.nblk = pl.nblk;
+    k.cap = reinterpret_cast<const double *>(ws + pl.o_cap);
+    k.eta = reinterpret_cast<const double *>(ws + pl.o_eta);
+    k.shift = reinterpret_cast<const int32_t *>(ws + pl.o_shift);
+    k.partials = reinterpret_cast<uint64_t *>(ws + pl.o_part);
+    k.tickets = reinterpret_cast<uint32_t *>(ws + pl.o_tick);
+    k.flags = reinterpret_cast<int32_t *>(ws + pl.o_flags);
+    k.status = reinterpret_cast<int32_t *>(ws + pl.o_status);
+    k.skip_mask = kFlagError;
+    *out = c;
+    return ESP_OK;
+}
+
+esp_status esp_score_select(esp_ctx *c, const double *prices, int32_t *choice, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (prices == nullptr || choice == nullptr) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = dev(launch_prepare(c->pl.R, prices, c->base.flags, nullptr, c->base.status, c->pl.B, s))) != ESP_OK)
+        return st;
+    KArgs a = c->base;
+    a.lam_in = prices;
+    a.choice = choice;
+    a.reduce = 0;
+    a.skip_mask = kFlagError;
+    return dev(launch_select(c, a, s));
+}
+
+esp_status esp_reduce_demand(esp_ctx *c, const int32_t *choice, double *demand, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (choice == nullptr || demand == nullptr) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    KArgs a = c->base;
+    a.choice_in = choice;
+    a.demand_out = demand;
+    a.skip_mask = 0;
+    a.reduce = 1;
+    return dev(launch_gather(c->pl.R, a, c->pl.B, s));
+}
+
+esp_status esp_update_prices(esp_ctx *c, const double *demand, int32_t t, double *prices, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (demand == nullptr || prices == nullptr || t < 1) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = stage_eta(c, t, 1, s)) != ESP_OK) return st;
+    KArgs a = c->base;
+    a.lam_in = prices;
+    a.lam_out = prices;
+    return dev(launch_update(c->pl.R, a, demand, c->pl.B, s));
+}
+
+esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start, double tol, int32_t *choice,
+                     double *demand, const esp_trace *trace, int32_t *iters_done, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (prices == nullptr || iters < 0 || t_start < 1 || !(tol >= 0.0) || !std::isfinite(tol))
+        return ESP_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(t_start) + iters - 1 > INT32_MAX) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
+    int32_t *d_iters = reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters);
+    if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.status, B, s))) != ESP_OK) return st;
+    for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
+        const int n = std::min<int32_t>(kEtaChunk, iters - i0);
+        if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
+        for (int i = 0; i < n; ++i) {
+            const int64_t it = static_cast<int64_t>(i0) + i;
+            KArgs a = c->base;
+            a.lam_in = prices;
+            a.lam_out = prices;
+            a.eta = c->base.eta + static_cast<size_t>(i) * B;
+            a.skip_mask = kFlagError | kFlagStopped;
+            a.iters_done = d_iters;
+            a.iter_no = static_cast<int32_t>(it + 1);
+            a.tol = tol;
+            a.reduce = 1;
+            if (trace) {
+                if (trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(it) * B * R;
+                if (trace->demand) a.tr_U = trace->demand + static_cast<size_t>(it) * B * R;
+                if (trace->choice) a.choice = trace->choice + static_cast<size_t>(it) * B * N;
+            }
+            if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
+        }
+    }
+    // Re-selection at the final prices (no update).
+    if (choice || demand) {
+        KArgs a = c->base;
+        a.lam_in = prices;
+        a.choice = choice;
+        a.demand_out = demand;
+        a.skip_mask = kFlagError;
+        a.reduce = demand ? 1 : 0;
+        if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
+    }
+    if (iters_done &&
+        hipMemcpyAsync(iters_done, d_iters, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return ESP_ERR_DEVICE;
+    return ESP_OK;
+}
+
+esp_status esp_device_status(esp_ctx *c, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (hipStreamSynchronize(s) != hipSuccess) return ESP_ERR_DEVICE;
+    int32_t v = 0, zero = 0;
+    int32_t *d = reinterpret_cast<int32_t *>(c->ws + c->pl.o_status);
+    if (hipMemcpy(&v, d, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return ESP_ERR_DEVICE;
+    if (hipMemcpy(d, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return ESP_ERR_DEVICE;
+    return static_cast<esp_status>(v);
+}
+
+esp_status esp_destroy(esp_ctx *c) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (c->eta_pending) (void)hipEventSynchronize(c->eta_ev);
+    if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
+    if (c->h_eta) (void)hipHostFree(c->h_eta);
+    c->magic = 0;
+    delete c;
+    return ESP_OK;
+}
+
+}  // extern "C"

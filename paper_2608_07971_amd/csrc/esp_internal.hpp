@@ -1,0 +1,86 @@
+// Internal definitions shared by the host driver and the gfx950 kernels of the
+// Elastic Shadow Pricing library.  Not part of the public ABI (include/esp.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace esp {
+
+// A tile is what one wavefront scores per step: 64 lanes x 4 table entries,
+// read with one 128-bit load per lane per column.
+constexpr int kTileEntries = 256;
+constexpr int kWaveSize = 64;
+constexpr int kBlockThreads = 256;                  // 4 wavefronts per workgroup
+constexpr int kBlockWaves = kBlockThreads / kWaveSize;
+constexpr int kMaxR = 8;
+constexpr int kMaxFamily = 256;                     // configurations per job
+constexpr int kEtaChunk = 1024;                     // iterations of step sizes staged at once
+
+// Flags per cluster (device int32).
+constexpr int kFlagStopped = 1;                     // converged under tol: skip further updates
+constexpr int kFlagError = 2;                       // invalid prices: skip everything
+
+// Device status codes (mirror esp_status values).
+constexpr int kStatusNonfinite = 3;
+constexpr int kStatusInvalid = 1;
+constexpr int kStatusRange = 7;
+
+// Tile metadata of the CSR layout: bit i of `head` is set when table slot i of
+// the tile starts a job; `first_job` is the job owning slot 0.
+struct TileMeta {
+    uint32_t head[8];
+    uint32_t first_job;
+    uint32_t pad[7];
+};
+static_assert(sizeof(TileMeta) == 64, "tile metadata is one 64-byte line");
+
+// Where job j's family starts in its cluster's columns, and its size.
+struct JobSlot {
+    uint32_t slot;
+    uint32_t size;
+};
+
+// Arguments of the select/demand/update kernels (passed by value).
+struct KArgs {
+    const float *table;            // SoA image: cluster b, column a (0 = utility, 1+r = demand r)
+                                   // starts at table + b * cluster_stride + a * col_len
+    size_t cluster_stride;         // floats between clusters = (R + 1) * col_len
+    size_t col_len;                // floats per column = tiles * 256
+    const TileMeta *meta;          // CSR only: [tiles]
+    const JobSlot *jobs;           // [N] slot of each family (used by the gather kernel)
+    int32_t N;                     // jobs per cluster
+    int32_t K;                     // dense family size (0 for CSR)
+    int32_t tiles;                 // tiles per cluster
+    int32_t nblk;                  // workgroups per cluster
+    const double *lam_in;          // [B][R] prices at which to select
+    double *lam_out;               // [B][R] updated prices, or NULL (no update)
+    const double *cap;             // [B][R] capacities
+    const double *eta;             // [B] step sizes of this iteration (when lam_out != NULL)
+    const int32_t *shift;          // [B][R] fixed-point window (lowest bit exponent) per column
+    uint64_t *partials;            // [B][nblk][R][2] per-workgroup 128-bit sums
+    uint32_t *tickets;             // [B] arrival counters (0 between launches)
+    int32_t *flags;                // [B] per-cluster run flags
+    int32_t skip_mask;             // skip a cluster when (flags[b] & skip_mask) != 0
+    int32_t *status;               // first device-detected error
+    int32_t *choice;               // [B][N] output, or NULL
+    const int32_t *choice_in;      // [B][N] input of the gather kernel
+    double *demand_out;            // [B][R] output U, or NULL
+    double *tr_lam;                // [B][R] trace row for lambda^{t+1}, or NULL
+    double *tr_U;                  // [B][R] trace row for U^t, or NULL
+    int32_t *iters_done;           // [B] or NULL
+    int32_t iter_no;               // updates made including this one (1-based)
+    double tol;                    // > 0 enables the stop test
+    int32_t reduce;                // 0: select only (no demand, no ticket)
+};
+
+// Host-side launchers (esp_kernels.hip).
+hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
+hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,
+                          int32_t *status, int B, hipStream_t s);
+
+}  // namespace esp

@@ -1,0 +1,460 @@
+// gfx950 kernels of the Elastic Shadow Pricing hot path (paper Sec. 3.2).
+//
+// One price iteration = one launch of a fused kernel:
+//   score   s_jk = u_jk - sum_r lambda_r d_jkr          (Sec. 3.2.2, bracket of Eq. 6)
+//   select  c_j  = argmax_k s_jk, lowest k on ties     (Sec. 3.2.2 per-job subproblem)
+//   demand  U_r  = sum_j d_{j,c_j,r}, exact             (Sec. 3.2.3, under Eq. 8)
+//   update  lambda_r <- max(0, lambda_r + eta_t (U_r - C_r)) in the last
+//           workgroup of each cluster                   (Eq. 8)
+//
+// Table layout (built by the packer): per cluster, one fp32 column for the
+// utility and one per resource, each a sequence of 256-entry tiles.  A
+// wavefront scores one tile per step with one 128-bit load per lane per
+// column (lane l holds entries 4l .. 4l+3 of the tile).
+//
+// Arithmetic contract: binary64, no contraction (`fp contract(off)` below and
+// -ffp-contract=off on the command line), rent summed left to right over r.
+// The demand sum is exact: each fp32 demand is turned into a 128-bit integer
+// multiple of 2^shift (the column's lowest set bit, fixed by the packer),
+// integers are added in any order, and the total is rounded once to binary64
+// (round-to-nearest-even).  No floating-point atomics are used.
+#include "esp_internal.hpp"
+
+#pragma clang fp contract(off)
+
+namespace esp {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned __int128 u128;
+
+// ---------------------------------------------------------------------------
+// Wavefront primitives
+// ---------------------------------------------------------------------------
+
+// DPP lane moves inside 16-lane rows.
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // lane i <- lane 7-i within each 8 lanes
+constexpr int kDppMirror = 0x140;       // lane i <- lane 15-i within each row
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = dpp_i<CTRL>(static_cast<int>(static_cast<unsigned>(b)));
+    const int hi = dpp_i<CTRL>(static_cast<int>(b >> 32));
+    return __longlong_as_double(static_cast<long long>(
+        (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+
+// (os, ok) replaces (s, k) when its score is larger, or equal with a lower
+// configuration index.  This is a total order on (score, -index) for the
+// non-NaN scores the kernels produce, so any reduction tree returns the
+// entry a sequential lowest-index scan would.
+__device__ __forceinline__ void take_better(double &s, int &k, double os, int ok) {
+    const bool b = (os > s) || (os == s && ok < k);
+    s = b ? os : s;
+    k = b ? ok : k;
+}
+
+// Argmax over aligned groups of LPJ lanes (LPJ in {1,2,4,8,16}); afterwards
+// every lane of a group holds the group's winner.
+template <int LPJ>
+__device__ __forceinline__ void group_argmax(double &s, int &k) {
+    if constexpr (LPJ >= 2) take_better(s, k, dpp_d<kDppXor1>(s), dpp_i<kDppXor1>(k));
+    if constexpr (LPJ >= 4) take_better(s, k, dpp_d<kDppXor2>(s), dpp_i<kDppXor2>(k));
+    if constexpr (LPJ >= 8) take_better(s, k, dpp_d<kDppHalfMirror>(s), dpp_i<kDppHalfMirror>(k));
+    if constexpr (LPJ >= 16) take_better(s, k, dpp_d<kDppMirror>(s), dpp_i<kDppMirror>(k));
+}
+
+// Compiler-level ordering of LDS traffic inside one wavefront.
+__device__ __forceinline__ void wave_sync() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// ---------------------------------------------------------------------------
+// Exact fixed-point demand accumulation
+// ---------------------------------------------------------------------------
+
+// v (finite, +0.0 or positive) as an integer multiple of 2^sh.  The packer
+// guarantees that every nonzero value of the column has its lowest set bit at
+// or above 2^sh and its highest below 2^(sh + 127 - ceil(log2 N)), so the
+// shift is exact and N of them cannot overflow 128 bits.
+__device__ __forceinline__ u128 fx_of(float v, int sh) {
+    const uint32_t bits = __float_as_uint(v);
+    const uint32_t e = bits >> 23;
+    const uint32_t m = (bits & 0x7fffffu) | (e ? 0x800000u : 0u);
+    int s = (e ? static_cast<int>(e) : 1) - 150 - sh;
+    if (m == 0) return 0;
+    s = s > 127 ? 127 : (s < -127 ? -127 : s);
+    const u128 mm = m;
+    return s >= 0 ? (mm << s) : (mm >> (-s));
+}
+
+// Round a * 2^sh to the nearest binary64, ties to even.
+__device__ __forceinline__ double fx_to_double(u128 a, int sh) {
+    if (a == 0) return 0.0;
+    const uint64_t hi = static_cast<uint64_t>(a >> 64);
+    const uint64_t lo = static_cast<uint64_t>(a);
+    const int h = hi ? 127 - __clzll(hi) : 63 - __clzll(lo);
+    if (h <= 52) return ldexp(static_cast<double>(lo), sh);
+    const int drop = h - 52;
+    uint64_t m = static_cast<uint64_t>(a >> drop);
+    const u128 rem = a & ((static_cast<u128>(1) << drop) - 1);
+    const u128 half = static_cast<u128>(1) << (drop - 1);
+    if (rem > half || (rem == half && (m & 1u))) m += 1;   // m <= 2^53: exact as a double
+    return ldexp(static_cast<double>(m), drop + sh);
+}
+
+// ---------------------------------------------------------------------------
+// Cluster completion: per-workgroup sums -> last workgroup -> U, Eq. 8 update
+// ---------------------------------------------------------------------------
+
+// bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
+template <int R>
+__device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum) {
+    __shared__ int s_last;
+    __shared__ u128 s_red[kBlockThreads];
+    __shared__ int s_ok[R];
+    const int t = threadIdx.x;
+    if (t < R) {
+        uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + blk) * R + t) * 2;
+        const u128 v = bsum[t];
+        p[0] = static_cast<uint64_t>(v);
+        p[1] = static_cast<uint64_t>(v >> 64);
+        __threadfence();                       // release the partial to every XCD
+    }
+    __syncthreads();
+    if (t == 0) {
+        const unsigned prev = atomicAdd(&a.tickets[cl], 1u);
+        s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();                           // acquire every workgroup's partial
+
+    // Sum the nblk partials of each resource: thread (g, r) takes blocks g, g+G, ...
+    constexpr int G = kBlockThreads / R;
+    u128 s = 0;
+    if (t < G * R) {
+        const int r = t % R, g = t / R;
+#pragma unroll 1
+        for (int b = g; b < a.nblk; b += G) {
+            const uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + b) * R + r) * 2;
+            s += (static_cast<u128>(p[1]) << 64) | p[0];
+        }
+    }
+    s_red[t] = s;
+    __syncthreads();
+    if (t < R) {
+        u128 tot = 0;
+#pragma unroll 1
+        for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
+        bool bad = a.flags && (a.flags[cl] & 4);
+        double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + t]);
+        if (a.demand_out) a.demand_out[cl * R + t] = U;
+        if (a.tr_U) a.tr_U[cl * R + t] = U;
+        int ok = 1;
+        if (a.lam_out) {
+            const double lo = a.lam_in[cl * R + t];
+            const double g = U - a.cap[cl * R + t];
+            const double x = lo + a.eta[cl] * g;
+            const double ln = (x > 0.0) ? x : 0.0;
+            a.lam_out[cl * R + t] = ln;
+            if (a.tr_lam) a.tr_lam[cl * R + t] = ln;
+            const double diff = fabs(ln - lo);
+            const double scale = lo > 1.0 ? lo : 1.0;
+            ok = diff <= a.tol * scale;
+        }
+        s_ok[t] = ok;
+    }
+    __syncthreads();
+    if (t == 0) {
+        a.tickets[cl] = 0u;                    // ready for the next launch
+        if (a.flags && (a.flags[cl] & 4)) a.flags[cl] &= ~4;
+        if (a.lam_out) {
+            if (a.iters_done) a.iters_done[cl] = a.iter_no;
+            int all = 1;
+            for (int r = 0; r < R; ++r) all &= s_ok[r];
+            if (a.tol > 0.0 && all && a.flags) a.flags[cl] |= kFlagStopped;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Dense families: K = 4 * LPJ configurations per job, LPJ lanes per job
+// ---------------------------------------------------------------------------
+
+template <int R, int LPJ>
+__global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
+    constexpr int JPT = kWaveSize / LPJ;       // jobs per tile
+    constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
+    __shared__ float s_stage[kBlockWaves][JPT][R];
+    __shared__ u128 s_acc[kBlockThreads];
+    __shared__ u128 s_wsum[kBlockWaves][R];
+    __shared__ u128 s_bsum[R];
+
+    const int cl = blockIdx.x / a.nblk;
+    const int blk = blockIdx.x - cl * a.nblk;
+    if (a.flags && (a.flags[cl] & a.skip_mask)) return;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    double lam[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) lam[r] = a.lam_in[cl * R + r];
+
+    const float *col = a.table + cl * a.cluster_stride;
+    const int my_r = lane % R;
+    const int my_q = lane / R;
+    const bool acc_lane = lane < Q * R;
+    const int my_shift = a.shift[cl * R + my_r];
+    const int gl = lane % LPJ;                 // lane within its job group
+    const int jt = lane / LPJ;                 // job within the tile
+    u128 acc = 0;
+
+    const int stride = a.nblk * kBlockWaves;
+    for (int tile = blk * kBlockWaves + wave; tile < a.tiles; tile += stride) {
+        const size_t base = static_cast<size_t>(tile) * kTileEntries + lane * 4;
+        const f4 u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(col + base));
+        f4 d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(col + (r + 1) * a.col_len + base));
+
+        double best = 0.0;
+        int bi = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            double rent = static_cast<double>(d[0][i]) * lam[0];
+#pragma unroll
+            for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
+            const double s = static_cast<double>(u[i]) - rent;
+            if (i == 0 || s > best) { best = s; bi = i; }
+        }
+        int k = gl * 4 + bi;
+        group_argmax<LPJ>(best, k);
+        const int j = tile * JPT + jt;
+        const bool owner = (k >> 2) == gl;     // this lane holds the winning entry
+        if (a.choice && owner && j < a.N) a.choice[static_cast<size_t>(cl) * a.N + j] = k;
+        if (a.reduce) {
+            if (owner) {
+                const int w = k & 3;
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    const float v = (w == 0) ? d[r][0] : (w == 1) ? d[r][1] : (w == 2) ? d[r][2] : d[r][3];
+                    s_stage[wave][jt][r] = (j < a.N) ? v : 0.0f;
+                }
+            }
+            wave_sync();
+            if (acc_lane) {
+#pragma unroll 1
+                for (int q = my_q; q < JPT; q += Q) acc += fx_of(s_stage[wave][q][my_r], my_shift);
+            }
+            wave_sync();
+        }
+    }
+    if (!a.reduce) return;
+
+    // Workgroup sum per resource (integer adds: any order gives the same value).
+    s_acc[threadIdx.x] = acc_lane ? acc : static_cast<u128>(0);
+    __syncthreads();
+    if (threadIdx.x < kBlockWaves * R) {
+        const int w = threadIdx.x / R, r = threadIdx.x % R;
+        u128 v = 0;
+#pragma unroll 1
+        for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
+        s_wsum[w][r] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < R) {
+        u128 v = 0;
+#pragma unroll 1
+        for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
+        s_bsum[threadIdx.x] = v;
+    }
+    __syncthreads();
+    finish_cluster<R>(a, cl, blk, s_bsum);
+}
+
+// ---------------------------------------------------------------------------
+// Gather: U from caller-supplied choices (granular esp_reduce_demand)
+// ---------------------------------------------------------------------------
+
+template <int R>
+__global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
+    __shared__ u128 s_red[kBlockThreads];
+    __shared__ u128 s_bsum[R];
+    __shared__ int s_bad;
+    const int cl = blockIdx.x / a.nblk;
+    const int blk = blockIdx.x - cl * a.nblk;
+    const float *col = a.table + cl * a.cluster_stride;
+    u128 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0;
+    int sh[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) sh[r] = a.shift[cl * R + r];
+    if (threadIdx.x == 0) s_bad = 0;
+    __syncthreads();
+    bool bad = false;
+    for (int j = blk * kBlockThreads + threadIdx.x; j < a.N; j += a.nblk * kBlockThreads) {
+        const int c = a.choice_in[static_cast<size_t>(cl) * a.N + j];
+        uint32_t slot, size;
+        if (a.K > 0) {
+            slot = static_cast<uint32_t>(j) * static_cast<uint32_t>(a.K);
+            size = static_cast<uint32_t>(a.K);
+        } else {
+            slot = a.jobs[j].slot;
+            size = a.jobs[j].size;
+        }
+        if (c < 0 || static_cast<uint32_t>(c) >= size) { bad = true; continue; }
+        const size_t e = static_cast<size_t>(slot) + static_cast<uint32_t>(c);
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] += fx_of(col[(r + 1) * a.col_len + e], sh[r]);
+    }
+    if (bad) s_bad = 1;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        s_red[threadIdx.x] = acc[r];
+        __syncthreads();
+#pragma unroll 1
+        for (int st = kBlockThreads / 2; st > 0; st >>= 1) {
+            if (threadIdx.x < st) s_red[threadIdx.x] += s_red[threadIdx.x + st];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) s_bsum[r] = s_red[0];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0 && s_bad) {
+        atomicOr(&a.flags[cl], 4);
+        atomicCAS(a.status, 0, kStatusInvalid);
+    }
+    finish_cluster<R>(a, cl, blk, s_bsum);
+}
+
+// ---------------------------------------------------------------------------
+// Granular price update (esp_update_prices) and price validation
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bool price_ok(double x) {
+    return x >= 0.0 && x <= 0x1p400;            // false for NaN and +-Inf
+}
+
+template <int R>
+__global__ void k_update(KArgs a, const double *demand_in, int B) {
+    const int cl = blockIdx.x * blockDim.x + threadIdx.x;
+    if (cl >= B) return;
+    bool ok = true;
+    for (int r = 0; r < R; ++r) {
+        const double U = demand_in[cl * R + r];
+        ok = ok && price_ok(a.lam_in[cl * R + r]) && (U >= -0x1p200 && U <= 0x1p200);
+    }
+    if (!ok) {
+        atomicCAS(a.status, 0, kStatusNonfinite);
+        return;
+    }
+    for (int r = 0; r < R; ++r) {
+        const double lo = a.lam_in[cl * R + r];
+        const double g = demand_in[cl * R + r] - a.cap[cl * R + r];
+        const double x = lo + a.eta[cl] * g;
+        a.lam_out[cl * R + r] = (x > 0.0) ? x : 0.0;
+    }
+}
+
+// Validate prices before a solve or a selection; mark bad clusters.
+template <int R>
+__global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status, int B) {
+    const int cl = blockIdx.x * blockDim.x + threadIdx.x;
+    if (cl >= B) return;
+    bool ok = true;
+    for (int r = 0; r < R; ++r) ok = ok && price_ok(lam[cl * R + r]);
+    flags[cl] = ok ? 0 : kFlagError;
+    if (iters_done) iters_done[cl] = 0;
+    if (!ok) atomicCAS(status, 0, kStatusNonfinite);
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (runtime R / LPJ -> template instance)
+// ---------------------------------------------------------------------------
+
+template <int R>
+static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
+    switch (lpj) {
+        case 1: hipLaunchKernelGGL((k_dense<R, 1>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_dense<R, 2>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_dense<R, 4>), grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL((k_dense<R, 8>), grid, block, 0, s, a); break;
+        case 16: hipLaunchKernelGGL((k_dense<R, 16>), grid, block, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+#define ESP_DISPATCH_R(R, CALL)              \
+    switch (R) {                             \
+        case 1: return CALL(1);              \
+        case 2: return CALL(2);              \
+        case 3: return CALL(3);              \
+        case 4: return CALL(4);              \
+        case 5: return CALL(5);              \
+        case 6: return CALL(6);              \
+        case 7: return CALL(7);              \
+        case 8: return CALL(8);              \
+        default: return hipErrorInvalidValue; \
+    }
+
+hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_dense_r<RR>(lpj, a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_gather_r(const KArgs &a, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_gather<R>), dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_gather_r<RR>(a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_update_r(const KArgs &a, const double *demand_in, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_update<R>), dim3((B + 255) / 256), dim3(256), 0, s, a, demand_in, B);
+    return hipGetLastError();
+}
+
+hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s) {
+#define CALL(RR) launch_update_r<RR>(a, demand_in, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_prepare_r(const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status,
+                                   int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, lam, flags, iters_done, status, B);
+    return hipGetLastError();
+}
+
+hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status,
+                          int B, hipStream_t s) {
+#define CALL(RR) launch_prepare_r<RR>(lam, flags, iters_done, status, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+hipError_t launch_csr(int, const KArgs &, int, hipStream_t) { return hipErrorNotSupported; }
+
+}  // namespace esp

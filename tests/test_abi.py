@@ -1,0 +1,140 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry
+point declared in include/esp.h, and rejects bad arguments on the host before
+any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2608_07971_amd as esp
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "esp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(esp_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert {"esp_create", "esp_score_select", "esp_reduce_demand", "esp_update_prices", "esp_solve"} <= set(names)
+    L = esp.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(esp._SIGS), "binding and header disagree"
+
+
+def test_status_strings():
+    for code in range(10):
+        assert esp.status_string(code)
+    assert esp.status_string(0) == "ok"
+
+
+def _ws(p, opt=None):
+    return esp.esp_workspace_size(p, opt)
+
+
+def test_workspace_size_dense_and_csr():
+    t = workloads.make("tiny")
+    n1 = _ws(esp.Problem.from_instance(t))
+    assert n1 >= t.table_bytes()
+    r = workloads.make("ragged", n_jobs=5000)
+    n2 = _ws(esp.Problem.from_instance(r))
+    assert n2 >= r.table_bytes()
+    L = workloads.make("large", n_jobs=1000)
+    assert _ws(esp.Problem.from_instance(L)) >= L.table_bytes()
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("num_resources", 0, esp.ESP_ERR_SHAPE), ("num_resources", 9, esp.ESP_ERR_SHAPE),
+    ("num_jobs", 0, esp.ESP_ERR_SHAPE), ("num_clusters", 0, esp.ESP_ERR_SHAPE),
+    ("configs_per_job", 0, esp.ESP_ERR_SHAPE), ("configs_per_job", 257, esp.ESP_ERR_SHAPE),
+])
+def test_workspace_size_shape_errors(field, value, code):
+    p = esp.Problem.from_instance(workloads.make("tiny"))
+    setattr(p.c, field, value)
+    with pytest.raises(esp.EspError) as e:
+        _ws(p)
+    assert e.value.code == code
+
+
+def test_bad_offsets_and_options():
+    inst = workloads.random_small(1, 10, 5, 2)
+    p = esp.Problem.from_instance(inst)
+    p.offsets[3] = p.offsets[2]                       # empty family
+    with pytest.raises(esp.EspError) as e:
+        _ws(p)
+    assert e.value.code == esp.ESP_ERR_SHAPE
+    p2 = esp.Problem.from_instance(inst)
+    opt = esp.esp_options(0)
+    opt.reserved[2] = 1
+    with pytest.raises(esp.EspError) as e:
+        _ws(p2, opt)
+    assert e.value.code == esp.ESP_ERR_INVALID_ARG
+    with pytest.raises(esp.EspError):
+        _ws(p2, esp.esp_options(-1))
+
+
+class _FakeWs:
+    """Stands in for a workspace tensor in host-side rejection tests."""
+    def __init__(self, ptr, n):
+        self.ptr, self.n = ptr, n
+
+    def numel(self):
+        return self.n
+
+    def element_size(self):
+        return 1
+
+
+def _create(inst, rule=None, eta0=None, ws_ptr=0, ws_n=0):
+    p = esp.Problem.from_instance(inst)
+    e0 = np.ascontiguousarray(inst.eta0 if eta0 is None else eta0, dtype=np.float64)
+    step = esp.esp_step_rule(inst.rule if rule is None else rule, e0.ctypes.data)
+    out = C.c_void_p(None)
+    code = esp.lib().esp_create(C.addressof(p.c), C.addressof(step), None, ws_ptr or None, ws_n, None,
+                                C.byref(out))
+    return code, out.value
+
+
+def test_create_rejects_bad_values_on_host():
+    base = workloads.random_small(2, 8, 4, 3)
+    nan_u = workloads.random_small(2, 8, 4, 3); nan_u.utility[0, 5] = np.nan
+    inf_d = workloads.random_small(2, 8, 4, 3); inf_d.demand[0, 3, 1] = np.inf
+    neg_d = workloads.random_small(2, 8, 4, 3); neg_d.demand[0, 3, 1] = -1.0
+    nan_c = workloads.random_small(2, 8, 4, 3); nan_c.capacity[0, 0] = np.nan
+    big_c = workloads.random_small(2, 8, 4, 3); big_c.capacity[0, 0] = 2.0 ** 300
+    masked = workloads.random_small(2, 8, 4, 3)
+    masked.feasible = np.ones((1, masked.nnz), np.uint8)
+    masked.feasible[0, masked.offsets[2]:masked.offsets[3]] = 0
+    wide = workloads.random_small(2, 8, 4, 3); wide.demand[0, 0, 0] = 1e-38; wide.demand[0, 1, 0] = 1e38
+    assert _create(nan_u)[0] == esp.ESP_ERR_NONFINITE
+    assert _create(inf_d)[0] == esp.ESP_ERR_NONFINITE
+    assert _create(neg_d)[0] == esp.ESP_ERR_NEGATIVE_DEMAND
+    assert _create(nan_c)[0] == esp.ESP_ERR_NONFINITE
+    assert _create(big_c)[0] == esp.ESP_ERR_RANGE
+    assert _create(masked)[0] == esp.ESP_ERR_EMPTY_FAMILY
+    assert _create(wide)[0] == esp.ESP_ERR_RANGE
+    assert _create(base, rule=7)[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(base, eta0=[0.0])[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(base, eta0=[np.inf])[0] == esp.ESP_ERR_NONFINITE
+    assert _create(base, eta0=[2.0 ** 101])[0] == esp.ESP_ERR_RANGE
+    # valid problem, missing / misaligned / short workspace
+    assert _create(base)[0] == esp.ESP_ERR_WORKSPACE
+    assert _create(base, ws_ptr=4096 + 8, ws_n=1 << 30)[0] == esp.ESP_ERR_WORKSPACE
+    assert _create(base, ws_ptr=4096, ws_n=16)[0] == esp.ESP_ERR_WORKSPACE
+
+
+def test_null_context_is_rejected():
+    L = esp.lib()
+    assert L.esp_solve(None, None, 1, 1, 0.0, None, None, None, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_score_select(None, None, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_reduce_demand(None, None, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_update_prices(None, None, 1, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_device_status(None, None) == esp.ESP_ERR_STATE
+    assert L.esp_destroy(None) == esp.ESP_ERR_STATE

@@ -1,0 +1,184 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle.
+
+Choices must be bit-exact; demand sums and prices must agree within 1e-9
+relative (they are in fact bitwise equal: both sides round the exact demand
+sum once).  Every case prints its name before touching the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_07971_amd as esp
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+REL = 1e-9
+
+
+def _say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def _close(gpu, ref, floor=0.0):
+    gpu, ref = np.asarray(gpu), np.asarray(ref)
+    tol = REL * np.maximum(np.maximum(np.abs(gpu), np.abs(ref)), floor)
+    return bool(np.all(np.abs(gpu - ref) <= tol))
+
+
+def _check_trace(g, ref, n_iters):
+    ch = g["tr_choice"].cpu().numpy()[:n_iters]
+    assert np.array_equal(ch, ref["tr_choice"][:n_iters]), "per-iterate choices differ"
+    U, lam = g["tr_U"].cpu().numpy()[:n_iters], g["tr_lam"].cpu().numpy()[:n_iters]
+    assert _close(U, ref["tr_U"][:n_iters]) and _close(lam, ref["tr_lam"][:n_iters])
+    # the exact demand sum makes them bitwise equal
+    assert np.array_equal(U, ref["tr_U"][:n_iters])
+    assert np.array_equal(lam, ref["tr_lam"][:n_iters])
+    assert np.array_equal(g["choice"].cpu().numpy(), ref["choice"])
+    assert np.array_equal(g["U"].cpu().numpy(), ref["U"])
+    assert np.array_equal(g["lam"].cpu().numpy(), ref["lam"])
+
+
+DENSE_CASES = {
+    "tiny": lambda: workloads.make("tiny"),
+    "small": lambda: workloads.make("small"),
+    "large_4099": lambda: workloads.make("large", n_jobs=4099),                 # ragged tail tile
+    "batched_3x515": lambda: workloads.make("batched", n_jobs=515, n_clusters=3),
+    "k4_r1": lambda: workloads.random_small(5, 301, 4, 1, dense=True, iters=80),
+    "k16_r3": lambda: workloads.random_small(6, 777, 16, 3, dense=True, iters=80),
+    "k64_r8_dyadic": lambda: workloads.random_small(7, 130, 64, 8, dense=True, dyadic=True, iters=80,
+                                                    rule=workloads.STEP_CONST),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DENSE_CASES))
+def test_free_running_trace_matches_oracle(name):
+    inst = DENSE_CASES[name]()
+    T = min(inst.iters, 120)
+    _say(f"free-running {name} B={inst.B} N={inst.N} K={inst.dense_k} R={inst.R} T={T}")
+    s = esp.Solver(inst)
+    g = s.solve(s.prices(inst.lam0), T, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
+    _check_trace(g, ref, T)
+    assert (g["iters_done"].cpu().numpy() == T).all()
+    assert s.device_status() == 0
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "large_4099", "batched_3x515"])
+def test_teacher_forced_select(name):
+    """esp_score_select at the oracle's own prices lambda^t returns the
+    oracle's choices bitwise, for every sampled t."""
+    inst = DENSE_CASES[name]()
+    T = min(inst.iters, 60)
+    _say(f"teacher-forced {name}")
+    ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
+    lams = np.concatenate([inst.lam0[None], ref["tr_lam"][:-1]], axis=0)
+    s = esp.Solver(inst)
+    for t in sorted({0, 1, 2, T // 2, T - 1}):
+        ch = s.score_select(s.prices(lams[t])).cpu().numpy()
+        assert np.array_equal(ch, ref["tr_choice"][t]), t
+
+
+@pytest.mark.parametrize("name", ["tiny", "batched_3x515", "k16_r3"])
+def test_granular_equals_fused(name):
+    """score_select -> reduce_demand -> update_prices, driven from the host,
+    reproduces esp_solve's trace bitwise."""
+    inst = DENSE_CASES[name]()
+    T = 25
+    _say(f"granular {name}")
+    s = esp.Solver(inst)
+    g = s.solve(s.prices(inst.lam0), T, trace=True, trace_choice=True)
+    lam = s.prices(inst.lam0)
+    for i in range(T):
+        ch = s.score_select(lam)
+        U = s.reduce_demand(ch)
+        s.update_prices(U, i + 1, lam)
+        torch.cuda.synchronize()
+        assert torch.equal(ch, g["tr_choice"][i])
+        assert torch.equal(U, g["tr_U"][i])
+        assert torch.equal(lam, g["tr_lam"][i])
+    assert s.device_status() == 0
+
+
+def test_run_to_run_and_geometry_determinism():
+    """Same inputs, different workgroup counts: bitwise identical results
+    (integer demand sums do not depend on the reduction tree)."""
+    inst = workloads.make("large", n_jobs=6000)
+    T = 40
+    _say("determinism large_6000")
+    outs = []
+    for nb in (0, 0, 1, 3, 64):
+        s = esp.Solver(inst, blocks_per_cluster=nb)
+        g = s.solve(s.prices(inst.lam0), T, trace=True)
+        torch.cuda.synchronize()
+        outs.append((g["tr_lam"].cpu().numpy(), g["tr_U"].cpu().numpy(), g["choice"].cpu().numpy()))
+        s.close()
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert np.array_equal(a, b)
+
+
+def test_warm_start_continues_bitwise():
+    inst = workloads.make("small")
+    _say("warm start small")
+    s = esp.Solver(inst)
+    full = s.solve(s.prices(inst.lam0), 90, trace=True)
+    lam = s.prices(inst.lam0)
+    a = s.solve(lam, 40, trace=True)
+    b = s.solve(lam, 50, t_start=41, trace=True)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([a["tr_lam"], b["tr_lam"]]), full["tr_lam"])
+    assert torch.equal(b["choice"], full["choice"])
+
+
+def test_early_stop_matches_oracle():
+    inst = workloads.random_small(18, 10, 4, 2, dense=True, iters=500, eta0=0.02)
+    _say("early stop")
+    tol = 1e-3
+    ref = oracle.Oracle(inst).solve(tol=tol, trace_choice=True)
+    s = esp.Solver(inst)
+    g = s.solve(s.prices(inst.lam0), inst.iters, tol=tol, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    n = int(ref["iters_done"][0])
+    assert n < inst.iters
+    assert int(g["iters_done"].cpu()[0]) == n
+    _check_trace(g, ref, n)
+
+
+def test_mask_never_selected():
+    inst = workloads.random_small(21, 200, 8, 3, dense=True, iters=60)
+    rng = np.random.default_rng(3)
+    mask = (rng.random((1, inst.nnz)) < 0.6).astype(np.uint8)
+    mask.reshape(200, 8)[:, 5] = 1
+    inst.feasible = mask
+    _say("feasibility mask")
+    ref = oracle.Oracle(inst).solve(trace_choice=True)
+    s = esp.Solver(inst)
+    g = s.solve(s.prices(inst.lam0), inst.iters, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    _check_trace(g, ref, inst.iters)
+
+
+def test_device_errors_are_reported():
+    inst = workloads.make("tiny")
+    _say("device errors")
+    s = esp.Solver(inst)
+    bad = s.prices(np.full((1, 4), np.nan))
+    s.solve(bad, 5)
+    assert s.device_status() == esp.ESP_ERR_NONFINITE
+    assert s.device_status() == 0                      # cleared
+    neg = s.prices(np.array([[0.1, -1.0, 0.0, 0.0]]))
+    s.score_select(neg)
+    assert s.device_status() == esp.ESP_ERR_NONFINITE
+    ch = torch.zeros((1, inst.N), dtype=torch.int32, device="cuda")
+    ch[0, 7] = 8                                       # outside the family of 8
+    U = s.reduce_demand(ch)
+    assert s.device_status() == esp.ESP_ERR_INVALID_ARG
+    assert torch.isnan(U).all()
+    ch[0, 7] = 3
+    U = s.reduce_demand(ch)
+    torch.cuda.synchronize()
+    assert not torch.isnan(U).any()
+    ref = oracle.Oracle(inst).demand_sum(0, ch.cpu().numpy()[0])
+    assert np.array_equal(U.cpu().numpy()[0], ref)
