@@ -35,6 +35,7 @@ def _parse():
     ap.add_argument("--config", default="large", choices=["tiny", "small", "large", "ragged", "batched"])
     ap.add_argument("--iters", type=int, default=0, help="override T (0 = the workload's own)")
     ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
+    ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_large.json"),
@@ -86,7 +87,7 @@ def main() -> int:
     T = args.iters or inst.iters
     print(f"[bench] {args.config}: B={inst.B} N={inst.N} R={inst.R} nnz={inst.nnz} T={T} "
           f"(generated in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
-    solver = esp.Solver(inst, "cuda:0", blocks_per_cluster=args.blocks)
+    solver = esp.Solver(inst, "cuda:0", blocks_per_cluster=args.blocks, sweep_order=args.sweep)
     stream = torch.cuda.Stream()
     lam0 = solver.prices(inst.lam0)
     lam = lam0.clone()

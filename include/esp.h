@@ -87,8 +87,11 @@ typedef struct {
 } esp_step_rule;
 
 typedef struct {
-    int32_t blocks_per_cluster;      /* 0 = chosen by the library from the problem size */
-    int32_t reserved[7];             /* must be zero */
+    int32_t blocks_per_cluster;      /* workgroups per cluster; 0 = one per compute unit over the device */
+    int32_t sweep_order;             /* 0 = alternate the table sweep direction every iteration (reuses
+                                        the memory-side cache), 1 = always front to back; results are
+                                        identical either way */
+    int32_t reserved[6];             /* must be zero */
 } esp_options;
 
 /* Optional per-iteration record of esp_solve (device pointers, iteration-major;

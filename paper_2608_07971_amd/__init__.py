@@ -52,7 +52,7 @@ class esp_step_rule(C.Structure):
 
 
 class esp_options(C.Structure):
-    _fields_ = [("blocks_per_cluster", C.c_int32), ("reserved", C.c_int32 * 7)]
+    _fields_ = [("blocks_per_cluster", C.c_int32), ("sweep_order", C.c_int32), ("reserved", C.c_int32 * 6)]
 
 
 class esp_trace(C.Structure):
@@ -204,13 +204,13 @@ class Solver:
     logical problem (offsets, utility, demand, capacity, feasible, eta0, rule,
     dense_k)."""
 
-    def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, stream=None):
+    def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, sweep_order: int = 0, stream=None):
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU: the ESP library has no CPU path")
         self.device = torch.device(device)
         self.problem = Problem.from_instance(inst)
         self.B, self.N, self.R = self.problem.B, self.problem.N, self.problem.R
-        self.options = esp_options(int(blocks_per_cluster))
+        self.options = esp_options(int(blocks_per_cluster), int(sweep_order))
         nbytes = esp_workspace_size(self.problem, self.options)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         with torch.cuda.device(self.device):

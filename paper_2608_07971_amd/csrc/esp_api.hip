@@ -40,6 +40,15 @@ struct Plan {
            o_tick = 0, o_flags = 0, o_iters = 0, o_status = 0, total = 0;
 };
 
+// Compute units of the current device (256 on MI355X); 256 when no device
+// can be queried (workspace sizing on a host without a GPU).
+int device_cus() {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+    return n;
+}
+
 bool dense_fast_k(int K) { return K == 4 || K == 8 || K == 16 || K == 32 || K == 64; }
 
 // Family sizes of the problem (dense or CSR) and validation of the offsets.
@@ -73,7 +82,8 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     if (p == nullptr) return ESP_ERR_INVALID_ARG;
     if (opt) {
         if (opt->blocks_per_cluster < 0) return ESP_ERR_INVALID_ARG;
-        for (int i = 0; i < 7; ++i)
+        if (opt->sweep_order != 0 && opt->sweep_order != 1) return ESP_ERR_INVALID_ARG;
+        for (int i = 0; i < 6; ++i)
             if (opt->reserved[i] != 0) return ESP_ERR_INVALID_ARG;
     }
     if (p->num_clusters < 1 || p->num_jobs < 1 || p->num_resources < 1 || p->num_resources > kMaxR)
@@ -110,10 +120,12 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     }
     pl->col_len = static_cast<size_t>(pl->tiles) * kTileEntries;
     if (pl->col_len >= (static_cast<size_t>(1) << 32)) return ESP_ERR_SHAPE;
-    // Workgroups: about 1024 in flight over the whole device, split across clusters.
+    // Workgroups: one per compute unit over the whole device, split across
+    // clusters (a persistent-style grid: every workgroup sweeps many tiles).
     const int max_useful = std::max(1, (pl->tiles + kBlockWaves - 1) / kBlockWaves);
+    const int cus = device_cus();
     int nblk = (opt && opt->blocks_per_cluster > 0) ? opt->blocks_per_cluster
-                                                     : std::max(1, (1024 + pl->B - 1) / pl->B);
+                                                     : std::max(1, (cus + pl->B - 1) / pl->B);
     pl->nblk = std::min(nblk, max_useful);
     if (static_cast<int64_t>(pl->nblk) * pl->B > INT32_MAX) return ESP_ERR_SHAPE;
 
@@ -170,6 +182,7 @@ struct esp_ctx {
     double *h_eta = nullptr;           // pinned staging for step sizes
     hipEvent_t eta_ev = nullptr;
     bool eta_pending = false;
+    int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
     KArgs base{};
 };
 
@@ -317,6 +330,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     c->rule = step->rule;
     c->eta0.assign(step->eta0, step->eta0 + B);
     c->ws = ws;
+    c->sweep = options ? options->sweep_order : 0;
     auto fail = [&](esp_status e) {
         if (c->h_eta) (void)hipHostFree(c->h_eta);
         if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
@@ -500,6 +514,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
             a.iter_no = static_cast<int32_t>(it + 1);
             a.tol = tol;
             a.reduce = 1;
+            a.reverse = (c->sweep == 0) ? static_cast<int32_t>(it & 1) : 0;
             if (trace) {
                 if (trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(it) * B * R;
                 if (trace->demand) a.tr_U = trace->demand + static_cast<size_t>(it) * B * R;
@@ -516,6 +531,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         a.demand_out = demand;
         a.skip_mask = kFlagError;
         a.reduce = demand ? 1 : 0;
+        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(iters & 1) : 0;
         if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
     }
     if (iters_done &&

@@ -73,6 +73,7 @@ struct KArgs {
     int32_t iter_no;               // updates made including this one (1-based)
     double tol;                    // > 0 enables the stop test
     int32_t reduce;                // 0: select only (no demand, no ticket)
+    int32_t reverse;               // sweep tiles back to front
 };
 
 // Host-side launchers (esp_kernels.hip).

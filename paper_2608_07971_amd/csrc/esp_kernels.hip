@@ -117,6 +117,12 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
 // ---------------------------------------------------------------------------
 
 // bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
+//
+// Ordering across the 8 XCDs (each with its own L2): the partials are plain
+// stores; thread 0 then takes a ticket with an agent-scope release atomic,
+// which writes the partials back past this XCD's L2.  Only the last workgroup
+// runs an agent-scope acquire (invalidating its stale lines) before it reads
+// the partials of every workgroup; the others never invalidate their L2.
 template <int R>
 __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum) {
     __shared__ int s_last;
@@ -128,26 +134,39 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         const u128 v = bsum[t];
         p[0] = static_cast<uint64_t>(v);
         p[1] = static_cast<uint64_t>(v >> 64);
-        __threadfence();                       // release the partial to every XCD
     }
     __syncthreads();
     if (t == 0) {
-        const unsigned prev = atomicAdd(&a.tickets[cl], 1u);
+        const unsigned prev =
+            __hip_atomic_fetch_add(&a.tickets[cl], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();                           // acquire every workgroup's partial
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-    // Sum the nblk partials of each resource: thread (g, r) takes blocks g, g+G, ...
+    // Sum the nblk partials of each resource: thread (g, r) takes blocks
+    // g, g+G, g+2G, ...; eight independent loads in flight per thread.
     constexpr int G = kBlockThreads / R;
+    constexpr int U = 8;
     u128 s = 0;
     if (t < G * R) {
         const int r = t % R, g = t / R;
+        const uint64_t *base = a.partials + (static_cast<size_t>(cl) * a.nblk * R + r) * 2;
 #pragma unroll 1
-        for (int b = g; b < a.nblk; b += G) {
-            const uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + b) * R + r) * 2;
-            s += (static_cast<u128>(p[1]) << 64) | p[0];
+        for (int b0 = g; b0 < a.nblk; b0 += U * G) {
+            u128 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int b = b0 + u * G;
+                v[u] = 0;
+                if (b < a.nblk) {
+                    const uint64_t *p = base + static_cast<size_t>(b) * R * 2;
+                    v[u] = (static_cast<u128>(p[1]) << 64) | p[0];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) s += v[u];
         }
     }
     s_red[t] = s;
@@ -220,13 +239,29 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     u128 acc = 0;
 
     const int stride = a.nblk * kBlockWaves;
-    for (int tile = blk * kBlockWaves + wave; tile < a.tiles; tile += stride) {
-        const size_t base = static_cast<size_t>(tile) * kTileEntries + lane * 4;
-        const f4 u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(col + base));
-        f4 d[R];
+    const size_t lane_off = static_cast<size_t>(lane) * 4;
+    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R]) {
+        const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
+        u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
         for (int r = 0; r < R; ++r)
-            d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(col + (r + 1) * a.col_len + base));
+            d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
+    };
+    // Tiles are swept front to back, or back to front when a.reverse is set
+    // (the loop alternates so that the tail just read is still in the
+    // memory-side cache); the exact demand sum does not depend on the order.
+    const int last = a.tiles - 1;
+    int tile = blk * kBlockWaves + wave;
+    f4 nu;
+    f4 nd[R];
+    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd);
+    for (; tile < a.tiles; tile += stride) {
+        const f4 u = nu;
+        f4 d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = nd[r];
+        if (tile + stride < a.tiles) load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd);
+        const int tl = a.reverse ? last - tile : tile;               // table tile scored now
 
         double best = 0.0;
         int bi = 0;
@@ -240,7 +275,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         }
         int k = gl * 4 + bi;
         group_argmax<LPJ>(best, k);
-        const int j = tile * JPT + jt;
+        const int j = tl * JPT + jt;
         const bool owner = (k >> 2) == gl;     // this lane holds the winning entry
         if (a.choice && owner && j < a.N) a.choice[static_cast<size_t>(cl) * a.N + j] = k;
         if (a.reduce) {

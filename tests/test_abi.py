@@ -73,11 +73,14 @@ def test_bad_offsets_and_options():
     p2 = esp.Problem.from_instance(inst)
     opt = esp.esp_options(0)
     opt.reserved[2] = 1
+    opt2 = esp.esp_options(0, 5)
     with pytest.raises(esp.EspError) as e:
         _ws(p2, opt)
     assert e.value.code == esp.ESP_ERR_INVALID_ARG
     with pytest.raises(esp.EspError):
         _ws(p2, esp.esp_options(-1))
+    with pytest.raises(esp.EspError):
+        _ws(p2, opt2)
 
 
 class _FakeWs:
