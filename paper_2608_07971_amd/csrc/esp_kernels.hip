@@ -319,6 +319,203 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// CSR families (ragged sizes 1..256): whole families packed into tiles
+// ---------------------------------------------------------------------------
+
+constexpr int kDppRowShr1 = 0x111;
+constexpr int kDppRowShr2 = 0x112;
+constexpr int kDppRowShr4 = 0x114;
+constexpr int kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+constexpr int kDppWaveShr1 = 0x138;
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_or_i(int old, int v) {
+    return __builtin_amdgcn_update_dpp(old, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_or_d(double old, double v) {
+    const long long ob = __double_as_longlong(old), vb = __double_as_longlong(v);
+    const int lo = dpp_or_i<CTRL, ROW_MASK>(static_cast<int>(static_cast<unsigned>(ob)),
+                                            static_cast<int>(static_cast<unsigned>(vb)));
+    const int hi = dpp_or_i<CTRL, ROW_MASK>(static_cast<int>(ob >> 32), static_cast<int>(vb >> 32));
+    return __longlong_as_double(static_cast<long long>(
+        (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+
+// One step of an inclusive segmented scan over lanes of (best score, slot,
+// segment-start flag): a lane without a segment start combines the value
+// arriving from lower lanes (lanes with no source receive the identity
+// (-inf, INT_MAX, 0)).  Lower slots come from lower lanes, so equal scores
+// keep the lower slot, as the sequential scan does.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
+    const double os = dpp_or_d<CTRL, ROW_MASK>(-__builtin_inf(), s);
+    const int ok = dpp_or_i<CTRL, ROW_MASK>(0x7fffffff, k);
+    const int of = dpp_or_i<CTRL, ROW_MASK>(0, f);
+    if (!f) {
+        take_better(s, k, os, ok);
+        f = of;
+    }
+}
+
+template <int R>
+__global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
+    __shared__ uint32_t s_win[kBlockWaves][8];
+    __shared__ u128 s_red[kBlockThreads];
+    __shared__ u128 s_bsum[R];
+
+    const int cl = blockIdx.x / a.nblk;
+    const int blk = blockIdx.x - cl * a.nblk;
+    if (a.flags && (a.flags[cl] & a.skip_mask)) return;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    double lam[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) lam[r] = a.lam_in[cl * R + r];
+    int sh[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) sh[r] = a.shift[cl * R + r];
+    u128 acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0;
+
+    const float *col = a.table + cl * a.cluster_stride;
+    const size_t lane_off = static_cast<size_t>(lane) * 4;
+    const int hshift = (lane & 7) * 4;                   // this lane's 4 head bits in its word
+    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R], uint32_t &hw) {
+        const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
+        u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
+        hw = a.meta[tl].head[lane >> 3];
+    };
+    const int stride = a.nblk * kBlockWaves;
+    const int last = a.tiles - 1;
+    int tile = blk * kBlockWaves + wave;
+    f4 nu;
+    f4 nd[R];
+    uint32_t nhw = 0;
+    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd, nhw);
+    for (; tile < a.tiles; tile += stride) {
+        const f4 u = nu;
+        f4 d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = nd[r];
+        const uint32_t hbits = (nhw >> hshift) & 0xFu;
+        if (tile + stride < a.tiles) load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd, nhw);
+        const int tl = a.reverse ? last - tile : tile;
+
+        double sc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            double rent = static_cast<double>(d[0][i]) * lam[0];
+#pragma unroll
+            for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
+            sc[i] = static_cast<double>(u[i]) - rent;
+        }
+        // Lane-local pass: the part before this lane's first head (it belongs to
+        // a segment from lower lanes), segments complete inside the lane, and
+        // the segment left open at the lane's end.
+        double pre_s = -__builtin_inf(), cur_s = -__builtin_inf();
+        int pre_k = 0x7fffffff, cur_k = 0x7fffffff;
+        bool has_pre = false, open = false;
+        uint32_t local_win = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int slot = lane * 4 + i;
+            if ((hbits >> i) & 1u) {
+                if (open) local_win |= 1u << (cur_k - lane * 4);
+                open = true;
+                cur_s = sc[i];
+                cur_k = slot;
+            } else if (open) {
+                if (sc[i] > cur_s) { cur_s = sc[i]; cur_k = slot; }
+            } else {
+                if (!has_pre || sc[i] > pre_s) { pre_s = sc[i]; pre_k = slot; }
+                has_pre = true;
+            }
+        }
+        const bool has_head = hbits != 0;
+        double ps = has_head ? cur_s : pre_s;
+        int pk = has_head ? cur_k : pre_k;
+        int pf = has_head ? 1 : 0;
+        seg_scan_step<kDppRowShr1, 0xf>(ps, pk, pf);
+        seg_scan_step<kDppRowShr2, 0xf>(ps, pk, pf);
+        seg_scan_step<kDppRowShr4, 0xf>(ps, pk, pf);
+        seg_scan_step<kDppRowShr8, 0xf>(ps, pk, pf);
+        seg_scan_step<kDppRowBcast15, 0xa>(ps, pk, pf);
+        seg_scan_step<kDppRowBcast31, 0xc>(ps, pk, pf);
+        // Value of the scan at the previous lane (the segment that ends inside this lane).
+        double qs = dpp_or_d<kDppWaveShr1, 0xf>(-__builtin_inf(), ps);
+        int qk = dpp_or_i<kDppWaveShr1, 0xf>(0x7fffffff, pk);
+
+        if (lane < 8) s_win[wave][lane] = 0u;
+        wave_sync();
+        if (local_win) atomicOr(&s_win[wave][lane >> 3], local_win << hshift);
+        if (has_head && lane > 0) {
+            if (has_pre) take_better(qs, qk, pre_s, pre_k);
+            atomicOr(&s_win[wave][qk >> 5], 1u << (qk & 31));
+        }
+        if (lane == kWaveSize - 1) atomicOr(&s_win[wave][pk >> 5], 1u << (pk & 31));
+        wave_sync();
+        const uint32_t wbits = (s_win[wave][lane >> 3] >> hshift) & 0xFu;
+        wave_sync();
+        if (wbits) {
+            uint32_t hw[8];
+            if (a.choice) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) hw[q] = a.meta[tl].head[q];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (!((wbits >> i) & 1u)) continue;
+                if (a.reduce) {
+#pragma unroll
+                    for (int r = 0; r < R; ++r) acc[r] += fx_of(d[r][i], sh[r]);
+                }
+                if (a.choice) {
+                    // job = first_job + (heads at or before the slot) - 1;
+                    // config = slot - (the last head at or before it)
+                    const int slot = lane * 4 + i;
+                    const int w = slot >> 5;
+                    int cnt = 0, hs = -1;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        uint32_t m = hw[q];
+                        if (q == w) m &= 0xffffffffu >> (31 - (slot & 31));
+                        if (q <= w) {
+                            cnt += __popc(m);
+                            if (m) hs = q * 32 + 31 - __clz(m);
+                        }
+                    }
+                    const int j = static_cast<int>(a.meta[tl].first_job) + cnt - 1;
+                    a.choice[static_cast<size_t>(cl) * a.N + j] = slot - hs;
+                }
+            }
+        }
+    }
+    if (!a.reduce) return;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        s_red[threadIdx.x] = acc[r];
+        __syncthreads();
+#pragma unroll 1
+        for (int st = kBlockThreads / 2; st > 0; st >>= 1) {
+            if (threadIdx.x < st) s_red[threadIdx.x] += s_red[threadIdx.x + st];
+            __syncthreads();
+        }
+        if (threadIdx.x == 0) s_bsum[r] = s_red[0];
+        __syncthreads();
+    }
+    finish_cluster<R>(a, cl, blk, s_bsum);
+}
+
+// ---------------------------------------------------------------------------
 // Gather: U from caller-supplied choices (granular esp_reduce_demand)
 // ---------------------------------------------------------------------------
 
@@ -490,6 +687,16 @@ hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *ite
 #undef CALL
 }
 
-hipError_t launch_csr(int, const KArgs &, int, hipStream_t) { return hipErrorNotSupported; }
+template <int R>
+static hipError_t launch_csr_r(const KArgs &a, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_csr<R>), dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_csr_r<RR>(a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
 
 }  // namespace esp

@@ -182,3 +182,103 @@ def test_device_errors_are_reported():
     assert not torch.isnan(U).any()
     ref = oracle.Oracle(inst).demand_sum(0, ch.cpu().numpy()[0])
     assert np.array_equal(U.cpu().numpy()[0], ref)
+
+
+# ---------------------------------------------------------------------------
+# CSR (ragged) families
+# ---------------------------------------------------------------------------
+
+def _extreme_families():
+    """Families of 1 and 256 configurations (a full tile) mixed with others."""
+    inst = workloads.random_small(31, 300, 9, 5, iters=60)
+    rng = np.random.default_rng(31)
+    K = rng.integers(1, 40, 300)
+    K[[0, 7, 8, 9, 150]] = 256
+    K[10:60] = 1
+    off = np.concatenate([[0], np.cumsum(K)]).astype(np.int64)
+    nnz = int(off[-1])
+    inst.offsets = off
+    inst.utility = (rng.random((1, nnz)) * 2).astype(np.float32)
+    inst.demand = (rng.random((1, nnz, 5)) * 4).astype(np.float32)
+    dd = inst.demand[0].astype(np.float64)
+    smin = np.minimum.reduceat(dd, off[:-1], axis=0).sum(axis=0)
+    smax = np.maximum.reduceat(dd, off[:-1], axis=0).sum(axis=0)
+    inst.capacity = (smin + 0.5 * (smax - smin))[None]
+    return inst
+
+
+CSR_CASES = {
+    "ragged_20000": lambda: workloads.make("ragged", n_jobs=20000),
+    "random_r1": lambda: workloads.random_small(41, 2000, 30, 1, iters=80),
+    "random_r8": lambda: workloads.random_small(42, 1500, 70, 8, iters=80),
+    "random_k3_dense_layout": lambda: workloads.random_small(43, 999, 3, 4, dense=True, iters=80),
+    "random_clusters_3": lambda: workloads.random_small(44, 700, 20, 3, n_clusters=3, iters=60),
+    "extreme_families": _extreme_families,
+    "ties_dyadic": lambda: workloads.random_small(45, 800, 12, 2, dyadic=True, iters=80,
+                                                  rule=workloads.STEP_CONST, eta0=0.125),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CSR_CASES))
+def test_csr_free_running_trace_matches_oracle(name):
+    inst = CSR_CASES[name]()
+    T = min(inst.iters, 120)
+    _say(f"csr free-running {name} B={inst.B} N={inst.N} nnz={inst.nnz} R={inst.R} T={T}")
+    s = esp.Solver(inst)
+    g = s.solve(s.prices(inst.lam0), T, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
+    _check_trace(g, ref, T)
+    assert s.device_status() == 0
+
+
+@pytest.mark.parametrize("name", ["hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt"])
+def test_hand_traces_on_gpu(name):
+    """The hand-derived worked examples (ties, projection to +0.0) on the GPU."""
+    from tests._helpers import golden_instance, read_golden
+    g = read_golden(name)
+    inst = golden_instance(g)
+    _say(f"hand trace {name}")
+    s = esp.Solver(inst)
+    out = s.solve(s.prices(inst.lam0), inst.iters, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    for i, row in enumerate(g["trace"]):
+        assert list(out["tr_choice"][i, 0].cpu().numpy()) == [int(x) for x in row[2]]
+        assert np.array_equal(out["tr_U"][i, 0].cpu().numpy(), np.array(row[3]))
+        assert np.array_equal(out["tr_lam"][i, 0].cpu().numpy(), np.array(row[4]))
+    assert list(out["choice"][0].cpu().numpy()) == [int(x) for x in g["final_choice"]]
+    assert np.array_equal(out["lam"][0].cpu().numpy(), np.array(g["final_lam"]))
+    assert not np.signbit(out["tr_lam"].cpu().numpy()).any()
+
+
+def test_csr_teacher_forced_and_granular():
+    inst = workloads.make("ragged", n_jobs=30000)
+    T = 30
+    _say("csr teacher-forced + granular ragged_30000")
+    ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
+    lams = np.concatenate([inst.lam0[None], ref["tr_lam"][:-1]], axis=0)
+    s = esp.Solver(inst)
+    for t in (0, 1, 15, T - 1):
+        ch = s.score_select(s.prices(lams[t]))
+        assert np.array_equal(ch.cpu().numpy(), ref["tr_choice"][t]), t
+        U = s.reduce_demand(ch)
+        assert np.array_equal(U.cpu().numpy(), ref["tr_U"][t])
+    lam = s.prices(lams[4])
+    s.update_prices(s.prices(ref["tr_U"][4]), 5, lam)
+    assert np.array_equal(lam.cpu().numpy(), ref["tr_lam"][4])
+
+
+def test_csr_mask_and_geometry():
+    inst = workloads.random_small(46, 3000, 25, 4, iters=50)
+    rng = np.random.default_rng(46)
+    mask = (rng.random((1, inst.nnz)) < 0.5).astype(np.uint8)
+    mask[0, inst.offsets[:-1]] = 1
+    inst.feasible = mask
+    _say("csr mask + geometry")
+    ref = oracle.Oracle(inst).solve(trace_choice=True)
+    for nb, sw in ((0, 0), (1, 1), (7, 0)):
+        s = esp.Solver(inst, blocks_per_cluster=nb, sweep_order=sw)
+        g = s.solve(s.prices(inst.lam0), inst.iters, trace=True, trace_choice=True)
+        torch.cuda.synchronize()
+        _check_trace(g, ref, inst.iters)
+        s.close()
