@@ -116,7 +116,10 @@ def main() -> int:
     sec = ms_total / 1e3
     configs = inst.B * inst.nnz
     launches = (T + 1) * args.steps                  # T fused iterations + the final re-selection
-    bytes_per_launch = configs * (1 + inst.R) * 4
+    # algorithmic bytes: the fp32 table read once per iteration, plus the
+    # family boundaries (one 4-byte offset per job) for ragged families
+    csr = inst.dense_k is None or inst.dense_k not in (4, 8, 16, 32, 64)
+    bytes_per_launch = configs * (1 + inst.R) * 4 + (4 * (inst.N + 1) if csr else 0)
     avg_launch_s = sec / launches
     achieved = bytes_per_launch / avg_launch_s / 1e9
     traffic = None
@@ -148,7 +151,7 @@ def main() -> int:
         "pct_hbm_peak": 100.0 * achieved / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_dense (fused score/select/demand/update)",
+                     "kernel": ("k_csr" if csr else "k_dense") + " (fused score/select/demand/update)",
                      "bytes_per_launch": bytes_per_launch, "avg_launch_us": avg_launch_s * 1e6},
     }
     if not args.no_cpu_baseline:

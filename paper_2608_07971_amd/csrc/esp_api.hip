@@ -297,8 +297,10 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
             }
     }
     // Fixed-point window per (cluster, resource): lowest set bit over the
-    // column; the highest bit plus log2(N) must stay below 2^127.
+    // column.  The highest bit plus log2(N + 1) fixes the accumulator width:
+    // 64-bit when it is at most 63 for every column, 128-bit when at most 127.
     std::vector<int32_t> shift(static_cast<size_t>(B) * R, 0);
+    int need_bits = 0;
     int lgN = 0;
     while ((static_cast<int64_t>(1) << lgN) < static_cast<int64_t>(N) + 1) ++lgN;
     for (int b = 0; b < B; ++b)
@@ -315,6 +317,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
             }
             if (lo == INT32_MAX) { shift[static_cast<size_t>(b) * R + r] = 0; continue; }
             if (hi - lo + lgN > 127) return ESP_ERR_RANGE;
+            need_bits = std::max(need_bits, hi - lo + lgN);
             shift[static_cast<size_t>(b) * R + r] = lo;
         }
 
@@ -445,6 +448,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.flags = reinterpret_cast<int32_t *>(ws + pl.o_flags);
     k.status = reinterpret_cast<int32_t *>(ws + pl.o_status);
     k.skip_mask = kFlagError;
+    k.acc128 = need_bits > 63 ? 1 : 0;
     *out = c;
     return ESP_OK;
 }

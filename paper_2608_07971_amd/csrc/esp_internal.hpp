@@ -74,6 +74,7 @@ struct KArgs {
     double tol;                    // > 0 enables the stop test
     int32_t reduce;                // 0: select only (no demand, no ticket)
     int32_t reverse;               // sweep tiles back to front
+    int32_t acc128;                // demand accumulators are 128-bit (else 64-bit)
 };
 
 // Host-side launchers (esp_kernels.hip).

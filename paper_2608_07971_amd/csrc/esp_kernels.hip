@@ -82,18 +82,21 @@ __device__ __forceinline__ void wave_sync() {
 // Exact fixed-point demand accumulation
 // ---------------------------------------------------------------------------
 
-// v (finite, +0.0 or positive) as an integer multiple of 2^sh.  The packer
-// guarantees that every nonzero value of the column has its lowest set bit at
-// or above 2^sh and its highest below 2^(sh + 127 - ceil(log2 N)), so the
-// shift is exact and N of them cannot overflow 128 bits.
-__device__ __forceinline__ u128 fx_of(float v, int sh) {
+// v (finite, +0.0 or positive) as an integer multiple of 2^sh in an
+// accumulator type A (64- or 128-bit, chosen by the packer per problem).  The
+// packer guarantees that every nonzero value of the column has its lowest set
+// bit at or above 2^sh and its highest below 2^(sh + bits(A) - 1 -
+// ceil(log2(N + 1))), so the shift is exact and N of them cannot overflow A.
+template <typename A>
+__device__ __forceinline__ A fx_of(float v, int sh) {
+    constexpr int kMax = static_cast<int>(sizeof(A)) * 8 - 1;
     const uint32_t bits = __float_as_uint(v);
     const uint32_t e = bits >> 23;
     const uint32_t m = (bits & 0x7fffffu) | (e ? 0x800000u : 0u);
     int s = (e ? static_cast<int>(e) : 1) - 150 - sh;
     if (m == 0) return 0;
-    s = s > 127 ? 127 : (s < -127 ? -127 : s);
-    const u128 mm = m;
+    s = s > kMax ? kMax : (s < -kMax ? -kMax : s);
+    const A mm = m;
     return s >= 0 ? (mm << s) : (mm >> (-s));
 }
 
@@ -118,32 +121,37 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
 
 // bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
 //
-// Ordering across the 8 XCDs (each with its own L2): the partials are plain
-// stores; thread 0 then takes a ticket with an agent-scope release atomic,
-// which writes the partials back past this XCD's L2.  Only the last workgroup
-// runs an agent-scope acquire (invalidating its stale lines) before it reads
-// the partials of every workgroup; the others never invalidate their L2.
+// Ordering across the 8 XCDs (each with its own L2) without cache-wide
+// writeback or invalidation: wavefront 0 publishes the partial with
+// agent-scope atomic exchanges, which are performed at the device coherence
+// point and have completed once their old values are back; it waits for them
+// (s_waitcnt vmcnt(0) on the returned values) before it takes a ticket with
+// an agent-scope atomic add.  The workgroup that draws the last ticket reads
+// every partial with agent-scope atomic loads, which bypass the non-coherent
+// caches.
 template <int R>
 __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum) {
     __shared__ int s_last;
     __shared__ u128 s_red[kBlockThreads];
     __shared__ int s_ok[R];
     const int t = threadIdx.x;
-    if (t < R) {
-        uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + blk) * R + t) * 2;
-        const u128 v = bsum[t];
-        p[0] = static_cast<uint64_t>(v);
-        p[1] = static_cast<uint64_t>(v >> 64);
-    }
-    __syncthreads();
-    if (t == 0) {
-        const unsigned prev =
-            __hip_atomic_fetch_add(&a.tickets[cl], 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
+    if (t < kWaveSize) {
+        uint64_t old = 0;
+        if (t < R) {
+            uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + blk) * R + t) * 2;
+            const u128 v = bsum[t];
+            old ^= __hip_atomic_exchange(p, static_cast<uint64_t>(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            old ^= __hip_atomic_exchange(p + 1, static_cast<uint64_t>(v >> 64), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" : : "v"(old) : "memory");
+        if (t == 0) {
+            const unsigned prev = __hip_atomic_fetch_add(&a.tickets[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
+        }
     }
     __syncthreads();
     if (!s_last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     // Sum the nblk partials of each resource: thread (g, r) takes blocks
     // g, g+G, g+2G, ...; eight independent loads in flight per thread.
@@ -161,8 +169,10 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
                 const int b = b0 + u * G;
                 v[u] = 0;
                 if (b < a.nblk) {
-                    const uint64_t *p = base + static_cast<size_t>(b) * R * 2;
-                    v[u] = (static_cast<u128>(p[1]) << 64) | p[0];
+                    uint64_t *p = const_cast<uint64_t *>(base) + static_cast<size_t>(b) * R * 2;
+                    const uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    v[u] = (static_cast<u128>(hi) << 64) | lo;
                 }
             }
 #pragma unroll
@@ -175,7 +185,7 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         u128 tot = 0;
 #pragma unroll 1
         for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
-        bool bad = a.flags && (a.flags[cl] & 4);
+        const bool bad = a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
         double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + t]);
         if (a.demand_out) a.demand_out[cl * R + t] = U;
         if (a.tr_U) a.tr_U[cl * R + t] = U;
@@ -210,7 +220,7 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
 // Dense families: K = 4 * LPJ configurations per job, LPJ lanes per job
 // ---------------------------------------------------------------------------
 
-template <int R, int LPJ>
+template <int R, int LPJ, typename A>
 __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     constexpr int JPT = kWaveSize / LPJ;       // jobs per tile
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
@@ -236,33 +246,24 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     const int my_shift = a.shift[cl * R + my_r];
     const int gl = lane % LPJ;                 // lane within its job group
     const int jt = lane / LPJ;                 // job within the tile
-    u128 acc = 0;
+    A acc = 0;
 
     const int stride = a.nblk * kBlockWaves;
     const size_t lane_off = static_cast<size_t>(lane) * 4;
-    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R]) {
+    // Tiles are swept front to back, or back to front when a.reverse is set;
+    // the exact demand sum does not depend on the order.
+    const int last = a.tiles - 1;
+    auto load_tile = [&](int t, f4 &u, f4 (&d)[R]) {
+        const int tl = a.reverse ? last - t : t;
         const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
         u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
         for (int r = 0; r < R; ++r)
             d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
     };
-    // Tiles are swept front to back, or back to front when a.reverse is set
-    // (the loop alternates so that the tail just read is still in the
-    // memory-side cache); the exact demand sum does not depend on the order.
-    const int last = a.tiles - 1;
-    int tile = blk * kBlockWaves + wave;
-    f4 nu;
-    f4 nd[R];
-    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd);
-    for (; tile < a.tiles; tile += stride) {
-        const f4 u = nu;
-        f4 d[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) d[r] = nd[r];
-        if (tile + stride < a.tiles) load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd);
-        const int tl = a.reverse ? last - tile : tile;               // table tile scored now
-
+    // Score, select and stage one tile held in registers.
+    auto process = [&](int t, const f4 &u, const f4 (&d)[R]) {
+        const int tl = a.reverse ? last - t : t;
         double best = 0.0;
         int bi = 0;
 #pragma unroll
@@ -270,35 +271,59 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             double rent = static_cast<double>(d[0][i]) * lam[0];
 #pragma unroll
             for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
-            const double s = static_cast<double>(u[i]) - rent;
-            if (i == 0 || s > best) { best = s; bi = i; }
+            const double sc = static_cast<double>(u[i]) - rent;
+            if (i == 0 || sc > best) { best = sc; bi = i; }
         }
         int k = gl * 4 + bi;
         group_argmax<LPJ>(best, k);
         const int j = tl * JPT + jt;
-        const bool owner = (k >> 2) == gl;     // this lane holds the winning entry
-        if (a.choice && owner && j < a.N) a.choice[static_cast<size_t>(cl) * a.N + j] = k;
+        const bool owner = ((k >> 2) == gl) && (j < a.N);   // this lane holds the winning entry
+        if (a.choice && owner) a.choice[static_cast<size_t>(cl) * a.N + j] = k;
         if (a.reduce) {
-            if (owner) {
-                const int w = k & 3;
+            const int w = k & 3;
+            float v[R];
 #pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const float v = (w == 0) ? d[r][0] : (w == 1) ? d[r][1] : (w == 2) ? d[r][2] : d[r][3];
-                    s_stage[wave][jt][r] = (j < a.N) ? v : 0.0f;
-                }
+            for (int r = 0; r < R; ++r) {
+                const float lo = (w & 1) ? d[r][1] : d[r][0];
+                const float hi = (w & 1) ? d[r][3] : d[r][2];
+                v[r] = (w & 2) ? hi : lo;
+            }
+            if (jt < JPT && !(j < a.N) && gl == 0) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) s_stage[wave][jt][r] = 0.0f;   // jobs past N add nothing
+            }
+            if (owner) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) s_stage[wave][jt][r] = v[r];
             }
             wave_sync();
             if (acc_lane) {
 #pragma unroll 1
-                for (int q = my_q; q < JPT; q += Q) acc += fx_of(s_stage[wave][q][my_r], my_shift);
+                for (int q = my_q; q < JPT; q += Q) acc += fx_of<A>(s_stage[wave][q][my_r], my_shift);
             }
             wave_sync();
         }
+    };
+    // Three register buffers, rotated by unrolling: while one tile is scored
+    // the loads of the next two are in flight (18 KB per wavefront at R = 8).
+    f4 ua, ub, uc;
+    f4 da[R], db[R], dc[R];
+    int tile = blk * kBlockWaves + wave;
+    if (tile < a.tiles) load_tile(tile, ua, da);
+    if (tile + stride < a.tiles) load_tile(tile + stride, ub, db);
+    for (; tile < a.tiles; tile += 3 * stride) {
+        const int t1 = tile + stride, t2 = tile + 2 * stride;
+        if (t2 < a.tiles) load_tile(t2, uc, dc);
+        process(tile, ua, da);
+        if (t2 + stride < a.tiles) load_tile(t2 + stride, ua, da);
+        if (t1 < a.tiles) process(t1, ub, db);
+        if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, ub, db);
+        if (t2 < a.tiles) process(t2, uc, dc);
     }
     if (!a.reduce) return;
 
     // Workgroup sum per resource (integer adds: any order gives the same value).
-    s_acc[threadIdx.x] = acc_lane ? acc : static_cast<u128>(0);
+    s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
     __syncthreads();
     if (threadIdx.x < kBlockWaves * R) {
         const int w = threadIdx.x / R, r = threadIdx.x % R;
@@ -361,10 +386,13 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
     }
 }
 
-template <int R>
+template <int R, typename A>
 __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
+    constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
     __shared__ uint32_t s_win[kBlockWaves][8];
-    __shared__ u128 s_red[kBlockThreads];
+    __shared__ float s_stage[kBlockWaves][kTileEntries][R];
+    __shared__ u128 s_acc[kBlockThreads];
+    __shared__ u128 s_wsum[kBlockWaves][R];
     __shared__ u128 s_bsum[R];
 
     const int cl = blockIdx.x / a.nblk;
@@ -376,12 +404,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     double lam[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) lam[r] = a.lam_in[cl * R + r];
-    int sh[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) sh[r] = a.shift[cl * R + r];
-    u128 acc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = 0;
+    const int my_r = lane % R;
+    const int my_q = lane / R;
+    const bool acc_lane = lane < Q * R;
+    const int my_shift = a.shift[cl * R + my_r];
+    A acc = 0;
 
     const float *col = a.table + cl * a.cluster_stride;
     const size_t lane_off = static_cast<size_t>(lane) * 4;
@@ -454,6 +481,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         double qs = dpp_or_d<kDppWaveShr1, 0xf>(-__builtin_inf(), ps);
         int qk = dpp_or_i<kDppWaveShr1, 0xf>(0x7fffffff, pk);
 
+        // Winner mask of the tile (one bit per slot), built in LDS.
         if (lane < 8) s_win[wave][lane] = 0u;
         wave_sync();
         if (local_win) atomicOr(&s_win[wave][lane >> 3], local_win << hshift);
@@ -463,8 +491,19 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         }
         if (lane == kWaveSize - 1) atomicOr(&s_win[wave][pk >> 5], 1u << (pk & 31));
         wave_sync();
-        const uint32_t wbits = (s_win[wave][lane >> 3] >> hshift) & 0xFu;
+        uint32_t wm[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) wm[q] = s_win[wave][q];
         wave_sync();
+        const uint32_t wbits = (wm[lane >> 3] >> hshift) & 0xFu;
+        // Rank of this lane's first winner among the tile's winners (slot order).
+        int rank = __popc(wm[lane >> 3] & ((1u << hshift) - 1u));
+        int n_win = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            n_win += __popc(wm[q]);
+            if (q < (lane >> 3)) rank += __popc(wm[q]);
+        }
         if (wbits) {
             uint32_t hw[8];
             if (a.choice) {
@@ -476,8 +515,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
                 if (!((wbits >> i) & 1u)) continue;
                 if (a.reduce) {
 #pragma unroll
-                    for (int r = 0; r < R; ++r) acc[r] += fx_of(d[r][i], sh[r]);
+                    for (int r = 0; r < R; ++r) s_stage[wave][rank][r] = d[r][i];
                 }
+                ++rank;
                 if (a.choice) {
                     // job = first_job + (heads at or before the slot) - 1;
                     // config = slot - (the last head at or before it)
@@ -498,20 +538,34 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
                 }
             }
         }
+        if (a.reduce) {
+            wave_sync();
+            if (acc_lane) {
+#pragma unroll 1
+                for (int q = my_q; q < n_win; q += Q) acc += fx_of<A>(s_stage[wave][q][my_r], my_shift);
+            }
+            wave_sync();
+        }
     }
     if (!a.reduce) return;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        s_red[threadIdx.x] = acc[r];
-        __syncthreads();
+
+    s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
+    __syncthreads();
+    if (threadIdx.x < kBlockWaves * R) {
+        const int w = threadIdx.x / R, r = threadIdx.x % R;
+        u128 v = 0;
 #pragma unroll 1
-        for (int st = kBlockThreads / 2; st > 0; st >>= 1) {
-            if (threadIdx.x < st) s_red[threadIdx.x] += s_red[threadIdx.x + st];
-            __syncthreads();
-        }
-        if (threadIdx.x == 0) s_bsum[r] = s_red[0];
-        __syncthreads();
+        for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
+        s_wsum[w][r] = v;
     }
+    __syncthreads();
+    if (threadIdx.x < R) {
+        u128 v = 0;
+#pragma unroll 1
+        for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
+        s_bsum[threadIdx.x] = v;
+    }
+    __syncthreads();
     finish_cluster<R>(a, cl, blk, s_bsum);
 }
 
@@ -519,7 +573,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
 // Gather: U from caller-supplied choices (granular esp_reduce_demand)
 // ---------------------------------------------------------------------------
 
-template <int R>
+template <int R, typename A>
 __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
     __shared__ u128 s_red[kBlockThreads];
     __shared__ u128 s_bsum[R];
@@ -527,7 +581,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
     const int cl = blockIdx.x / a.nblk;
     const int blk = blockIdx.x - cl * a.nblk;
     const float *col = a.table + cl * a.cluster_stride;
-    u128 acc[R];
+    A acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) acc[r] = 0;
     int sh[R];
@@ -549,12 +603,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
         if (c < 0 || static_cast<uint32_t>(c) >= size) { bad = true; continue; }
         const size_t e = static_cast<size_t>(slot) + static_cast<uint32_t>(c);
 #pragma unroll
-        for (int r = 0; r < R; ++r) acc[r] += fx_of(col[(r + 1) * a.col_len + e], sh[r]);
+        for (int r = 0; r < R; ++r) acc[r] += fx_of<A>(col[(r + 1) * a.col_len + e], sh[r]);
     }
     if (bad) s_bad = 1;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-        s_red[threadIdx.x] = acc[r];
+        s_red[threadIdx.x] = static_cast<u128>(acc[r]);
         __syncthreads();
 #pragma unroll 1
         for (int st = kBlockThreads / 2; st > 0; st >>= 1) {
@@ -616,18 +670,23 @@ __global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done
 // Launchers (runtime R / LPJ -> template instance)
 // ---------------------------------------------------------------------------
 
-template <int R>
-static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) {
+template <int R, typename A>
+static hipError_t launch_dense_ra(int lpj, const KArgs &a, int B, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
     switch (lpj) {
-        case 1: hipLaunchKernelGGL((k_dense<R, 1>), grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_dense<R, 2>), grid, block, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_dense<R, 4>), grid, block, 0, s, a); break;
-        case 8: hipLaunchKernelGGL((k_dense<R, 8>), grid, block, 0, s, a); break;
-        case 16: hipLaunchKernelGGL((k_dense<R, 16>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_dense<R, 1, A>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_dense<R, 2, A>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_dense<R, 4, A>), grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL((k_dense<R, 8, A>), grid, block, 0, s, a); break;
+        case 16: hipLaunchKernelGGL((k_dense<R, 16, A>), grid, block, 0, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+template <int R>
+static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) {
+    return a.acc128 ? launch_dense_ra<R, u128>(lpj, a, B, s) : launch_dense_ra<R, uint64_t>(lpj, a, B, s);
 }
 
 #define ESP_DISPATCH_R(R, CALL)              \
@@ -651,7 +710,11 @@ hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s) {
 
 template <int R>
 static hipError_t launch_gather_r(const KArgs &a, int B, hipStream_t s) {
-    hipLaunchKernelGGL((k_gather<R>), dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), 0, s, a);
+    const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
+    if (a.acc128)
+        hipLaunchKernelGGL((k_gather<R, u128>), grid, block, 0, s, a);
+    else
+        hipLaunchKernelGGL((k_gather<R, uint64_t>), grid, block, 0, s, a);
     return hipGetLastError();
 }
 
@@ -689,7 +752,11 @@ hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *ite
 
 template <int R>
 static hipError_t launch_csr_r(const KArgs &a, int B, hipStream_t s) {
-    hipLaunchKernelGGL((k_csr<R>), dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), 0, s, a);
+    const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
+    if (a.acc128)
+        hipLaunchKernelGGL((k_csr<R, u128>), grid, block, 0, s, a);
+    else
+        hipLaunchKernelGGL((k_csr<R, uint64_t>), grid, block, 0, s, a);
     return hipGetLastError();
 }
 
