@@ -38,6 +38,9 @@ def _parse():
     ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES (10 times): the reference kernel "
+                         "whose FETCH_SIZE / WRITE_SIZE counters scale the fused kernel's")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_large.json"),
                     help="HBM bytes per launch measured with rocprofv3 counters, if present")
     return ap.parse_args()
@@ -77,6 +80,16 @@ def main() -> int:
         return 2
     import numpy as np
     import torch
+
+    if args.calibrate_copy:
+        n = args.calibrate_copy // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4, "copies": 10}), flush=True)
+        return 0
 
     import paper_2608_07971_amd as esp
     import workloads
