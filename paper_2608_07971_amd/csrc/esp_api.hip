@@ -124,8 +124,10 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     // clusters (a persistent-style grid: every workgroup sweeps many tiles).
     const int max_useful = std::max(1, (pl->tiles + kBlockWaves - 1) / kBlockWaves);
     const int cus = device_cus();
+    // The CSR kernel does more VALU work per tile and runs two workgroups per CU.
+    const int per_cu = pl->csr ? 2 : 1;
     int nblk = (opt && opt->blocks_per_cluster > 0) ? opt->blocks_per_cluster
-                                                     : std::max(1, (cus + pl->B - 1) / pl->B);
+                                                     : std::max(1, (per_cu * cus + pl->B - 1) / pl->B);
     pl->nblk = std::min(nblk, max_useful);
     if (static_cast<int64_t>(pl->nblk) * pl->B > INT32_MAX) return ESP_ERR_SHAPE;
 

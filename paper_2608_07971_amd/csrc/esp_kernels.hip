@@ -119,6 +119,41 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
 // Cluster completion: per-workgroup sums -> last workgroup -> U, Eq. 8 update
 // ---------------------------------------------------------------------------
 
+// U_r from the cluster's exact total, the Eq. 8 update and the stop test for
+// resource r (one thread per resource of the cluster's last workgroup).
+template <int R>
+__device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r, u128 tot, int *s_ok) {
+    const bool bad = a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
+    const double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + r]);
+    if (a.demand_out) a.demand_out[cl * R + r] = U;
+    if (a.tr_U) a.tr_U[cl * R + r] = U;
+    int ok = 1;
+    if (a.lam_out) {
+        const double lo = a.lam_in[cl * R + r];
+        const double g = U - a.cap[cl * R + r];
+        const double x = lo + a.eta[cl] * g;
+        const double ln = (x > 0.0) ? x : 0.0;
+        a.lam_out[cl * R + r] = ln;
+        if (a.tr_lam) a.tr_lam[cl * R + r] = ln;
+        const double diff = fabs(ln - lo);
+        const double scale = lo > 1.0 ? lo : 1.0;
+        ok = diff <= a.tol * scale;
+    }
+    s_ok[r] = ok;
+}
+
+// Per-cluster bookkeeping after the update (thread 0 of the last workgroup).
+template <int R>
+__device__ __forceinline__ void complete_cluster(const KArgs &a, int cl, const int *s_ok) {
+    if (a.flags && (a.flags[cl] & 4)) a.flags[cl] &= ~4;
+    if (a.lam_out) {
+        if (a.iters_done) a.iters_done[cl] = a.iter_no;
+        int all = 1;
+        for (int r = 0; r < R; ++r) all &= s_ok[r];
+        if (a.tol > 0.0 && all && a.flags) a.flags[cl] |= kFlagStopped;
+    }
+}
+
 // bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
 //
 // Ordering across the 8 XCDs (each with its own L2) without cache-wide
@@ -135,6 +170,15 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
     __shared__ u128 s_red[kBlockThreads];
     __shared__ int s_ok[R];
     const int t = threadIdx.x;
+    if (a.nblk == 1) {
+        // One workgroup per cluster: its own sums are the totals.
+        if (t < R) s_red[t] = bsum[t];
+        __syncthreads();
+        if (t < R) complete_resource<R>(a, cl, t, s_red[t], s_ok);
+        __syncthreads();
+        if (t == 0) complete_cluster<R>(a, cl, s_ok);
+        return;
+    }
     if (t < kWaveSize) {
         uint64_t old = 0;
         if (t < R) {
@@ -185,34 +229,12 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         u128 tot = 0;
 #pragma unroll 1
         for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
-        const bool bad = a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
-        double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + t]);
-        if (a.demand_out) a.demand_out[cl * R + t] = U;
-        if (a.tr_U) a.tr_U[cl * R + t] = U;
-        int ok = 1;
-        if (a.lam_out) {
-            const double lo = a.lam_in[cl * R + t];
-            const double g = U - a.cap[cl * R + t];
-            const double x = lo + a.eta[cl] * g;
-            const double ln = (x > 0.0) ? x : 0.0;
-            a.lam_out[cl * R + t] = ln;
-            if (a.tr_lam) a.tr_lam[cl * R + t] = ln;
-            const double diff = fabs(ln - lo);
-            const double scale = lo > 1.0 ? lo : 1.0;
-            ok = diff <= a.tol * scale;
-        }
-        s_ok[t] = ok;
+        complete_resource<R>(a, cl, t, tot, s_ok);
     }
     __syncthreads();
     if (t == 0) {
         a.tickets[cl] = 0u;                    // ready for the next launch
-        if (a.flags && (a.flags[cl] & 4)) a.flags[cl] &= ~4;
-        if (a.lam_out) {
-            if (a.iters_done) a.iters_done[cl] = a.iter_no;
-            int all = 1;
-            for (int r = 0; r < R; ++r) all &= s_ok[r];
-            if (a.tol > 0.0 && all && a.flags) a.flags[cl] |= kFlagStopped;
-        }
+        complete_cluster<R>(a, cl, s_ok);
     }
 }
 
