@@ -36,6 +36,7 @@ def _parse():
     ap.add_argument("--iters", type=int, default=0, help="override T (0 = the workload's own)")
     ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
     ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
+    ap.add_argument("--mode", type=int, default=0, help="loop driver: 0 auto, 1 one launch per iteration, 2 persistent")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -100,7 +101,7 @@ def main() -> int:
     T = args.iters or inst.iters
     print(f"[bench] {args.config}: B={inst.B} N={inst.N} R={inst.R} nnz={inst.nnz} T={T} "
           f"(generated in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
-    solver = esp.Solver(inst, "cuda:0", blocks_per_cluster=args.blocks, sweep_order=args.sweep)
+    solver = esp.Solver(inst, "cuda:0", blocks_per_cluster=args.blocks, sweep_order=args.sweep, mode=args.mode)
     stream = torch.cuda.Stream()
     lam0 = solver.prices(inst.lam0)
     lam = lam0.clone()

@@ -56,6 +56,15 @@ typedef enum {
 /* Step rules of Eq. 8. */
 enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
 
+/* Loop drivers of esp_solve (results are identical in every mode). */
+enum {
+    ESP_MODE_AUTO = 0,        /* persistent when the table layout and the device allow it */
+    ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
+    ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; workgroups meet at a
+                                 per-cluster epoch after each price update (dense layouts only;
+                                 ESP_ERR_DEVICE when the grid cannot be co-resident) */
+};
+
 /* Opaque context: packed table + launch plan, created by esp_create. */
 typedef struct esp_ctx esp_ctx;
 
@@ -91,7 +100,8 @@ typedef struct {
     int32_t sweep_order;             /* 0 = alternate the table sweep direction every iteration (reuses
                                         the memory-side cache), 1 = always front to back; results are
                                         identical either way */
-    int32_t reserved[6];             /* must be zero */
+    int32_t mode;                    /* ESP_MODE_* loop driver of esp_solve */
+    int32_t reserved[5];             /* must be zero */
 } esp_options;
 
 /* Optional per-iteration record of esp_solve (device pointers, iteration-major;

@@ -32,6 +32,10 @@ ESP_ERR_STATE = 9
 ESP_STEP_CONST = 0
 ESP_STEP_INV_SQRT = 1
 
+ESP_MODE_AUTO = 0
+ESP_MODE_STREAM = 1
+ESP_MODE_PERSISTENT = 2
+
 
 class EspError(RuntimeError):
     def __init__(self, code: int, where: str):
@@ -52,7 +56,8 @@ class esp_step_rule(C.Structure):
 
 
 class esp_options(C.Structure):
-    _fields_ = [("blocks_per_cluster", C.c_int32), ("sweep_order", C.c_int32), ("reserved", C.c_int32 * 6)]
+    _fields_ = [("blocks_per_cluster", C.c_int32), ("sweep_order", C.c_int32), ("mode", C.c_int32),
+                ("reserved", C.c_int32 * 5)]
 
 
 class esp_trace(C.Structure):
@@ -204,13 +209,14 @@ class Solver:
     logical problem (offsets, utility, demand, capacity, feasible, eta0, rule,
     dense_k)."""
 
-    def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, sweep_order: int = 0, stream=None):
+    def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, sweep_order: int = 0,
+                 mode: int = ESP_MODE_AUTO, stream=None):
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU: the ESP library has no CPU path")
         self.device = torch.device(device)
         self.problem = Problem.from_instance(inst)
         self.B, self.N, self.R = self.problem.B, self.problem.N, self.problem.R
-        self.options = esp_options(int(blocks_per_cluster), int(sweep_order))
+        self.options = esp_options(int(blocks_per_cluster), int(sweep_order), int(mode))
         nbytes = esp_workspace_size(self.problem, self.options)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         with torch.cuda.device(self.device):

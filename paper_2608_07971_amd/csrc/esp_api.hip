@@ -37,7 +37,7 @@ struct Plan {
     int nblk = 0;       // workgroups per cluster
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_status = 0, total = 0;
+           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_status = 0, total = 0;
 };
 
 // Compute units of the current device (256 on MI355X); 256 when no device
@@ -83,7 +83,8 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     if (opt) {
         if (opt->blocks_per_cluster < 0) return ESP_ERR_INVALID_ARG;
         if (opt->sweep_order != 0 && opt->sweep_order != 1) return ESP_ERR_INVALID_ARG;
-        for (int i = 0; i < 6; ++i)
+        if (opt->mode < ESP_MODE_AUTO || opt->mode > ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
+        for (int i = 0; i < 5; ++i)
             if (opt->reserved[i] != 0) return ESP_ERR_INVALID_ARG;
     }
     if (p->num_clusters < 1 || p->num_jobs < 1 || p->num_resources < 1 || p->num_resources > kMaxR)
@@ -143,6 +144,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_tick = o;  o = align_up(o + B * sizeof(uint32_t));
     pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
     pl->o_iters = o; o = align_up(o + B * sizeof(int32_t));
+    pl->o_epoch = o; o = align_up(o + B * sizeof(uint32_t));
     pl->o_status = o; o = align_up(o + sizeof(int32_t));
     pl->total = o;
     return ESP_OK;
@@ -185,6 +187,7 @@ struct esp_ctx {
     hipEvent_t eta_ev = nullptr;
     bool eta_pending = false;
     int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
+    int mode = ESP_MODE_AUTO;
     KArgs base{};
 };
 
@@ -336,6 +339,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     c->eta0.assign(step->eta0, step->eta0 + B);
     c->ws = ws;
     c->sweep = options ? options->sweep_order : 0;
+    c->mode = options ? options->mode : ESP_MODE_AUTO;
     auto fail = [&](esp_status e) {
         if (c->h_eta) (void)hipHostFree(c->h_eta);
         if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
@@ -422,6 +426,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemsetAsync(ws + pl.o_tick, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_epoch, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess;
         if (ok && pl.csr)
             ok = hipMemcpyAsync(ws + pl.o_meta, meta.data(), sizeof(TileMeta) * meta.size(), hipMemcpyHostToDevice,
@@ -451,6 +456,10 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.status = reinterpret_cast<int32_t *>(ws + pl.o_status);
     k.skip_mask = kFlagError;
     k.acc128 = need_bits > 63 ? 1 : 0;
+    k.n_iters = 1;
+    k.B = B;
+    k.epoch = reinterpret_cast<uint32_t *>(ws + pl.o_epoch);
+    k.sweep_alt = c->sweep == 0 ? 1 : 0;
     *out = c;
     return ESP_OK;
 }
@@ -460,7 +469,8 @@ esp_status esp_score_select(esp_ctx *c, const double *prices, int32_t *choice, v
     if (st != ESP_OK) return st;
     if (prices == nullptr || choice == nullptr) return ESP_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if ((st = dev(launch_prepare(c->pl.R, prices, c->base.flags, nullptr, c->base.status, c->pl.B, s))) != ESP_OK)
+    if ((st = dev(launch_prepare(c->pl.R, prices, c->base.flags, nullptr, nullptr, c->base.status, c->pl.B, s))) !=
+        ESP_OK)
         return st;
     KArgs a = c->base;
     a.lam_in = prices;
@@ -505,28 +515,48 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
     int32_t *d_iters = reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters);
-    if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.status, B, s))) != ESP_OK) return st;
+    if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.epoch, c->base.status, B, s))) != ESP_OK)
+        return st;
+    // Persistent launches (one cooperative launch per chunk of up to
+    // kEtaChunk iterations) for dense tables; one launch per iteration
+    // otherwise, or when the device cannot hold the grid co-resident.
+    bool persistent = !c->pl.csr && c->mode != ESP_MODE_STREAM;
     for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
         const int n = std::min<int32_t>(kEtaChunk, iters - i0);
         if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
+        KArgs a = c->base;
+        a.lam_in = prices;
+        a.lam_out = prices;
+        a.skip_mask = kFlagError | kFlagStopped;
+        a.iters_done = d_iters;
+        a.tol = tol;
+        a.reduce = 1;
+        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i0 & 1) : 0;
+        a.iter_no = i0 + 1;
+        if (trace) {
+            if (trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(i0) * B * R;
+            if (trace->demand) a.tr_U = trace->demand + static_cast<size_t>(i0) * B * R;
+            if (trace->choice) a.choice = trace->choice + static_cast<size_t>(i0) * B * N;
+        }
+        if (persistent) {
+            a.n_iters = n;
+            a.epoch_base = static_cast<uint32_t>(i0);
+            const hipError_t e = launch_dense_persistent(R, c->pl.lpj, a, B, s);
+            if (e == hipSuccess) continue;
+            if (c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_DEVICE;
+            (void)hipGetLastError();
+            persistent = false;                // fall back to one launch per iteration
+        }
         for (int i = 0; i < n; ++i) {
-            const int64_t it = static_cast<int64_t>(i0) + i;
-            KArgs a = c->base;
-            a.lam_in = prices;
-            a.lam_out = prices;
-            a.eta = c->base.eta + static_cast<size_t>(i) * B;
-            a.skip_mask = kFlagError | kFlagStopped;
-            a.iters_done = d_iters;
-            a.iter_no = static_cast<int32_t>(it + 1);
-            a.tol = tol;
-            a.reduce = 1;
-            a.reverse = (c->sweep == 0) ? static_cast<int32_t>(it & 1) : 0;
-            if (trace) {
-                if (trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(it) * B * R;
-                if (trace->demand) a.tr_U = trace->demand + static_cast<size_t>(it) * B * R;
-                if (trace->choice) a.choice = trace->choice + static_cast<size_t>(it) * B * N;
-            }
-            if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
+            KArgs ai = a;
+            ai.n_iters = 1;
+            ai.eta = c->base.eta + static_cast<size_t>(i) * B;
+            ai.iter_no = i0 + i + 1;
+            ai.reverse = (c->sweep == 0) ? static_cast<int32_t>((i0 + i) & 1) : 0;
+            if (ai.tr_lam) ai.tr_lam = a.tr_lam + static_cast<size_t>(i) * B * R;
+            if (ai.tr_U) ai.tr_U = a.tr_U + static_cast<size_t>(i) * B * R;
+            if (ai.choice) ai.choice = a.choice + static_cast<size_t>(i) * B * N;
+            if ((st = dev(launch_select(c, ai, s))) != ESP_OK) return st;
         }
     }
     // Re-selection at the final prices (no update).

@@ -73,16 +73,28 @@ struct KArgs {
     int32_t iter_no;               // updates made including this one (1-based)
     double tol;                    // > 0 enables the stop test
     int32_t reduce;                // 0: select only (no demand, no ticket)
-    int32_t reverse;               // sweep tiles back to front
+    int32_t reverse;               // sweep tiles back to front (iteration 0 of the launch)
     int32_t acc128;                // demand accumulators are 128-bit (else 64-bit)
+    // Persistent launches run n_iters iterations; rows of eta / traces / the
+    // per-iteration choice advance by B, B*R and B*N per iteration, and the
+    // sweep direction alternates.  epoch[b] counts finished iterations.
+    int32_t n_iters;               // 1 for a single-iteration launch
+    int32_t B;                     // clusters
+    uint32_t *epoch;               // [B] (persistent launches)
+    uint32_t epoch_base;           // epoch value when this launch starts
+    int32_t sweep_alt;             // alternate the sweep direction between iterations
 };
+
+constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
 
 // Host-side launchers (esp_kernels.hip).
 hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
+// Cooperative launch (all workgroups co-resident) of a multi-iteration dense launch.
+hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,
-                          int32_t *status, int B, hipStream_t s);
+                          uint32_t *epoch, int32_t *status, int B, hipStream_t s);
 
 }  // namespace esp

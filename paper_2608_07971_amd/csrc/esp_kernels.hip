@@ -122,7 +122,8 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
 // U_r from the cluster's exact total, the Eq. 8 update and the stop test for
 // resource r (one thread per resource of the cluster's last workgroup).
 template <int R>
-__device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r, u128 tot, int *s_ok) {
+__device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r, u128 tot, int *s_ok,
+                                                  double *s_newlam) {
     const bool bad = a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
     const double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + r]);
     if (a.demand_out) a.demand_out[cl * R + r] = U;
@@ -133,8 +134,13 @@ __device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r,
         const double g = U - a.cap[cl * R + r];
         const double x = lo + a.eta[cl] * g;
         const double ln = (x > 0.0) ? x : 0.0;
-        a.lam_out[cl * R + r] = ln;
+        // agent-scope exchange: visible at the coherence point to the other
+        // workgroups of a persistent launch once it has returned
+        const double prev = __hip_atomic_exchange(&a.lam_out[cl * R + r], ln, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" : : "v"(prev) : "memory");
         if (a.tr_lam) a.tr_lam[cl * R + r] = ln;
+        s_newlam[r] = ln;
         const double diff = fabs(ln - lo);
         const double scale = lo > 1.0 ? lo : 1.0;
         ok = diff <= a.tol * scale;
@@ -143,15 +149,24 @@ __device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r,
 }
 
 // Per-cluster bookkeeping after the update (thread 0 of the last workgroup).
+// Returns whether the cluster stops (tol reached).
 template <int R>
-__device__ __forceinline__ void complete_cluster(const KArgs &a, int cl, const int *s_ok) {
-    if (a.flags && (a.flags[cl] & 4)) a.flags[cl] &= ~4;
+__device__ __forceinline__ int complete_cluster(const KArgs &a, int cl, const int *s_ok) {
+    int stop = 0;
+    if (a.flags && (a.flags[cl] & 4)) atomicAnd(&a.flags[cl], ~4);
     if (a.lam_out) {
-        if (a.iters_done) a.iters_done[cl] = a.iter_no;
+        // one writer per iteration, but not the same workgroup (or XCD) every
+        // time: a coherent exchange, so the last iteration's value is the one kept
+        if (a.iters_done) (void)__hip_atomic_exchange(&a.iters_done[cl], a.iter_no, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
         int all = 1;
         for (int r = 0; r < R; ++r) all &= s_ok[r];
-        if (a.tol > 0.0 && all && a.flags) a.flags[cl] |= kFlagStopped;
+        if (a.tol > 0.0 && all && a.flags) {
+            atomicOr(&a.flags[cl], kFlagStopped);
+            stop = 1;
+        }
     }
+    return stop;
 }
 
 // bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
@@ -164,8 +179,10 @@ __device__ __forceinline__ void complete_cluster(const KArgs &a, int cl, const i
 // an agent-scope atomic add.  The workgroup that draws the last ticket reads
 // every partial with agent-scope atomic loads, which bypass the non-coherent
 // caches.
+// s_newlam / s_stop (LDS) receive the new prices and the stop decision in
+// the last workgroup.
 template <int R>
-__device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum) {
+__device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum, double *s_newlam, int *s_stop) {
     __shared__ int s_last;
     __shared__ u128 s_red[kBlockThreads];
     __shared__ int s_ok[R];
@@ -174,10 +191,11 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         // One workgroup per cluster: its own sums are the totals.
         if (t < R) s_red[t] = bsum[t];
         __syncthreads();
-        if (t < R) complete_resource<R>(a, cl, t, s_red[t], s_ok);
+        if (t < R) complete_resource<R>(a, cl, t, s_red[t], s_ok, s_newlam);
         __syncthreads();
-        if (t == 0) complete_cluster<R>(a, cl, s_ok);
-        return;
+        if (t == 0) *s_stop = complete_cluster<R>(a, cl, s_ok);
+        __syncthreads();
+        return true;
     }
     if (t < kWaveSize) {
         uint64_t old = 0;
@@ -195,7 +213,7 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         }
     }
     __syncthreads();
-    if (!s_last) return;
+    if (!s_last) return false;
 
     // Sum the nblk partials of each resource: thread (g, r) takes blocks
     // g, g+G, g+2G, ...; eight independent loads in flight per thread.
@@ -229,13 +247,85 @@ __device__ void finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         u128 tot = 0;
 #pragma unroll 1
         for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
-        complete_resource<R>(a, cl, t, tot, s_ok);
+        complete_resource<R>(a, cl, t, tot, s_ok, s_newlam);
     }
     __syncthreads();
     if (t == 0) {
-        a.tickets[cl] = 0u;                    // ready for the next launch
-        complete_cluster<R>(a, cl, s_ok);
+        // ready for the next iteration
+        const unsigned o = __hip_atomic_exchange(&a.tickets[cl], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" : : "v"(o) : "memory");
+        *s_stop = complete_cluster<R>(a, cl, s_ok);
     }
+    return true;
+}
+
+// ---------------------------------------------------------------------------
+// Persistent launches: one launch runs n_iters iterations
+// ---------------------------------------------------------------------------
+
+// Per-iteration view of the arguments of a persistent launch.
+template <int R>
+__device__ __forceinline__ KArgs iteration_args(const KArgs &a, int it) {
+    KArgs ai = a;
+    const size_t i = static_cast<size_t>(it);
+    ai.eta = a.eta + i * a.B;
+    if (a.tr_lam) ai.tr_lam = a.tr_lam + i * a.B * R;
+    if (a.tr_U) ai.tr_U = a.tr_U + i * a.B * R;
+    if (a.choice) ai.choice = a.choice + i * a.B * a.N;
+    ai.iter_no = a.iter_no + it;
+    ai.reverse = a.reverse ^ (a.sweep_alt & it & 1);
+    return ai;
+}
+
+// After iteration `it` of a persistent launch: thread 0 of the last
+// workgroup has published the new prices (atomic exchanges) and reset the
+// ticket; it now bumps the cluster's epoch.  Every workgroup then waits for
+// the epoch (bounded: a timeout records an error and ends the launch) and
+// reads the new prices and the stop flag with agent-scope atomic loads.
+// Returns false when the workgroup must leave the iteration loop.
+template <int R>
+__device__ bool persist_barrier(const KArgs &a, int cl, int it, bool was_last, double *s_lam, int *s_go,
+                                const double *s_newlam, const int *s_stop) {
+    const int t = threadIdx.x;
+    if (a.nblk == 1) {
+        // The only workgroup of the cluster computed the prices itself.
+        __syncthreads();
+        if (*s_stop) return false;
+        if (t < R) s_lam[t] = s_newlam[t];
+        __syncthreads();
+        return true;
+    }
+    const uint32_t target = a.epoch_base + static_cast<uint32_t>(it) + 1u;
+    if (t == 0) {
+        if (was_last) {
+            asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // flag updates complete
+            __hip_atomic_fetch_add(&a.epoch[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        int go = 1;
+        // Bounded wait: about 2 s of the 100 MHz real-time counter, or until
+        // another workgroup has recorded an error.
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while (__hip_atomic_load(&a.epoch[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            __builtin_amdgcn_s_sleep(2);
+            if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+                __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
+                atomicCAS(a.status, 0, kStatusTimeout);
+                go = 0;
+                break;
+            }
+        }
+        if (go && a.flags &&
+            (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & (kFlagStopped | kFlagError)))
+            go = 0;
+        *s_go = go;
+    }
+    __syncthreads();
+    if (!*s_go) return false;
+    if (t < R)
+        s_lam[t] = __hip_atomic_load(const_cast<double *>(&a.lam_in[cl * R + t]), __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -250,12 +340,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     __shared__ u128 s_acc[kBlockThreads];
     __shared__ u128 s_wsum[kBlockWaves][R];
     __shared__ u128 s_bsum[R];
+    __shared__ double s_lam[R];
+    __shared__ double s_newlam[R];
+    __shared__ int s_go;
+    __shared__ int s_stop;
 
     const int cl = blockIdx.x / a.nblk;
     const int blk = blockIdx.x - cl * a.nblk;
     if (a.flags && (a.flags[cl] & a.skip_mask)) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (threadIdx.x == 0) s_stop = 0;
 
     double lam[R];
 #pragma unroll
@@ -272,11 +367,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
 
     const int stride = a.nblk * kBlockWaves;
     const size_t lane_off = static_cast<size_t>(lane) * 4;
-    // Tiles are swept front to back, or back to front when a.reverse is set;
-    // the exact demand sum does not depend on the order.
+    // Tiles are swept front to back, or back to front when `rev` is set; the
+    // exact demand sum does not depend on the order.
     const int last = a.tiles - 1;
-    auto load_tile = [&](int t, f4 &u, f4 (&d)[R]) {
-        const int tl = a.reverse ? last - t : t;
+    auto load_tile = [&](int t, int rev, f4 &u, f4 (&d)[R]) {
+        const int tl = rev ? last - t : t;
         const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
         u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
@@ -284,8 +379,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
     };
     // Score, select and stage one tile held in registers.
-    auto process = [&](int t, const f4 &u, const f4 (&d)[R]) {
-        const int tl = a.reverse ? last - t : t;
+    auto process = [&](const KArgs &ai, int t, const f4 &u, const f4 (&d)[R]) {
+        const int tl = ai.reverse ? last - t : t;
         double best = 0.0;
         int bi = 0;
 #pragma unroll
@@ -299,9 +394,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         int k = gl * 4 + bi;
         group_argmax<LPJ>(best, k);
         const int j = tl * JPT + jt;
-        const bool owner = ((k >> 2) == gl) && (j < a.N);   // this lane holds the winning entry
-        if (a.choice && owner) a.choice[static_cast<size_t>(cl) * a.N + j] = k;
-        if (a.reduce) {
+        const bool owner = ((k >> 2) == gl) && (j < ai.N);  // this lane holds the winning entry
+        if (ai.choice && owner) ai.choice[static_cast<size_t>(cl) * ai.N + j] = k;
+        if (ai.reduce) {
             const int w = k & 3;
             float v[R];
 #pragma unroll
@@ -310,7 +405,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
                 const float hi = (w & 1) ? d[r][3] : d[r][2];
                 v[r] = (w & 2) ? hi : lo;
             }
-            if (jt < JPT && !(j < a.N) && gl == 0) {
+            if (!(j < ai.N) && gl == 0) {
 #pragma unroll
                 for (int r = 0; r < R; ++r) s_stage[wave][jt][r] = 0.0f;   // jobs past N add nothing
             }
@@ -328,41 +423,56 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     };
     // Three register buffers, rotated by unrolling: while one tile is scored
     // the loads of the next two are in flight (18 KB per wavefront at R = 8).
+    // In a persistent launch the first two loads of the next iteration are
+    // issued before the wait for its prices.
     f4 ua, ub, uc;
     f4 da[R], db[R], dc[R];
-    int tile = blk * kBlockWaves + wave;
-    if (tile < a.tiles) load_tile(tile, ua, da);
-    if (tile + stride < a.tiles) load_tile(tile + stride, ub, db);
-    for (; tile < a.tiles; tile += 3 * stride) {
-        const int t1 = tile + stride, t2 = tile + 2 * stride;
-        if (t2 < a.tiles) load_tile(t2, uc, dc);
-        process(tile, ua, da);
-        if (t2 + stride < a.tiles) load_tile(t2 + stride, ua, da);
-        if (t1 < a.tiles) process(t1, ub, db);
-        if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, ub, db);
-        if (t2 < a.tiles) process(t2, uc, dc);
-    }
-    if (!a.reduce) return;
+    const int tile0 = blk * kBlockWaves + wave;
+    auto prefetch_two = [&](int rev) {
+        if (tile0 < a.tiles) load_tile(tile0, rev, ua, da);
+        if (tile0 + stride < a.tiles) load_tile(tile0 + stride, rev, ub, db);
+    };
+    prefetch_two(a.reverse);
+    for (int it = 0; it < a.n_iters; ++it) {
+        const KArgs ai = iteration_args<R>(a, it);
+        const int rev = ai.reverse;
+        for (int tile = tile0; tile < a.tiles; tile += 3 * stride) {
+            const int t1 = tile + stride, t2 = tile + 2 * stride;
+            if (t2 < a.tiles) load_tile(t2, rev, uc, dc);
+            process(ai, tile, ua, da);
+            if (t2 + stride < a.tiles) load_tile(t2 + stride, rev, ua, da);
+            if (t1 < a.tiles) process(ai, t1, ub, db);
+            if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, rev, ub, db);
+            if (t2 < a.tiles) process(ai, t2, uc, dc);
+        }
+        if (!ai.reduce) return;
 
-    // Workgroup sum per resource (integer adds: any order gives the same value).
-    s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
-    __syncthreads();
-    if (threadIdx.x < kBlockWaves * R) {
-        const int w = threadIdx.x / R, r = threadIdx.x % R;
-        u128 v = 0;
+        // Workgroup sum per resource (integer adds: any order gives the same value).
+        s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
+        acc = 0;
+        __syncthreads();
+        if (threadIdx.x < kBlockWaves * R) {
+            const int w = threadIdx.x / R, r = threadIdx.x % R;
+            u128 v = 0;
 #pragma unroll 1
-        for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
-        s_wsum[w][r] = v;
-    }
-    __syncthreads();
-    if (threadIdx.x < R) {
-        u128 v = 0;
+            for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
+            s_wsum[w][r] = v;
+        }
+        __syncthreads();
+        if (threadIdx.x < R) {
+            u128 v = 0;
 #pragma unroll 1
-        for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
-        s_bsum[threadIdx.x] = v;
+            for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
+            s_bsum[threadIdx.x] = v;
+        }
+        __syncthreads();
+        const bool was_last = finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+        if (it + 1 == a.n_iters) break;
+        prefetch_two(rev ^ a.sweep_alt);
+        if (!persist_barrier<R>(a, cl, it, was_last, s_lam, &s_go, s_newlam, &s_stop)) break;
+#pragma unroll
+        for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     }
-    __syncthreads();
-    finish_cluster<R>(a, cl, blk, s_bsum);
 }
 
 // ---------------------------------------------------------------------------
@@ -588,7 +698,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         s_bsum[threadIdx.x] = v;
     }
     __syncthreads();
-    finish_cluster<R>(a, cl, blk, s_bsum);
+    __shared__ double s_newlam[R];
+    __shared__ int s_stop;
+    finish_cluster<R>(a, cl, blk, s_bsum, s_newlam, &s_stop);
 }
 
 // ---------------------------------------------------------------------------
@@ -644,7 +756,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
         atomicOr(&a.flags[cl], 4);
         atomicCAS(a.status, 0, kStatusInvalid);
     }
-    finish_cluster<R>(a, cl, blk, s_bsum);
+    __shared__ double s_newlam[R];
+    __shared__ int s_stop;
+    finish_cluster<R>(a, cl, blk, s_bsum, s_newlam, &s_stop);
 }
 
 // ---------------------------------------------------------------------------
@@ -678,13 +792,15 @@ __global__ void k_update(KArgs a, const double *demand_in, int B) {
 
 // Validate prices before a solve or a selection; mark bad clusters.
 template <int R>
-__global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status, int B) {
+__global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch, int32_t *status,
+                          int B) {
     const int cl = blockIdx.x * blockDim.x + threadIdx.x;
     if (cl >= B) return;
     bool ok = true;
     for (int r = 0; r < R; ++r) ok = ok && price_ok(lam[cl * R + r]);
     flags[cl] = ok ? 0 : kFlagError;
     if (iters_done) iters_done[cl] = 0;
+    if (epoch) epoch[cl] = 0u;
     if (!ok) atomicCAS(status, 0, kStatusNonfinite);
 }
 
@@ -711,6 +827,27 @@ static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) 
     return a.acc128 ? launch_dense_ra<R, u128>(lpj, a, B, s) : launch_dense_ra<R, uint64_t>(lpj, a, B, s);
 }
 
+template <int R, typename A>
+static hipError_t launch_dense_coop_ra(int lpj, const KArgs &a, int B, hipStream_t s) {
+    const void *f = nullptr;
+    switch (lpj) {
+        case 1: f = reinterpret_cast<const void *>(&k_dense<R, 1, A>); break;
+        case 2: f = reinterpret_cast<const void *>(&k_dense<R, 2, A>); break;
+        case 4: f = reinterpret_cast<const void *>(&k_dense<R, 4, A>); break;
+        case 8: f = reinterpret_cast<const void *>(&k_dense<R, 8, A>); break;
+        case 16: f = reinterpret_cast<const void *>(&k_dense<R, 16, A>); break;
+        default: return hipErrorInvalidValue;
+    }
+    KArgs copy = a;
+    void *args[] = {&copy};
+    return hipLaunchCooperativeKernel(f, dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), args, 0, s);
+}
+
+template <int R>
+static hipError_t launch_dense_coop_r(int lpj, const KArgs &a, int B, hipStream_t s) {
+    return a.acc128 ? launch_dense_coop_ra<R, u128>(lpj, a, B, s) : launch_dense_coop_ra<R, uint64_t>(lpj, a, B, s);
+}
+
 #define ESP_DISPATCH_R(R, CALL)              \
     switch (R) {                             \
         case 1: return CALL(1);              \
@@ -726,6 +863,12 @@ static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) 
 
 hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s) {
 #define CALL(RR) launch_dense_r<RR>(lpj, a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_dense_coop_r<RR>(lpj, a, B, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }
@@ -759,15 +902,16 @@ hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, 
 }
 
 template <int R>
-static hipError_t launch_prepare_r(const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status,
-                                   int B, hipStream_t s) {
-    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, lam, flags, iters_done, status, B);
+static hipError_t launch_prepare_r(const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch,
+                                   int32_t *status, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, lam, flags, iters_done, epoch, status,
+                       B);
     return hipGetLastError();
 }
 
-hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done, int32_t *status,
-                          int B, hipStream_t s) {
-#define CALL(RR) launch_prepare_r<RR>(lam, flags, iters_done, status, B, s)
+hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch,
+                          int32_t *status, int B, hipStream_t s) {
+#define CALL(RR) launch_prepare_r<RR>(lam, flags, iters_done, epoch, status, B, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }

@@ -51,12 +51,16 @@ DENSE_CASES = {
 }
 
 
+MODES = {"stream": esp.ESP_MODE_STREAM, "persistent": esp.ESP_MODE_PERSISTENT}
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
 @pytest.mark.parametrize("name", sorted(DENSE_CASES))
-def test_free_running_trace_matches_oracle(name):
+def test_free_running_trace_matches_oracle(name, mode):
     inst = DENSE_CASES[name]()
     T = min(inst.iters, 120)
-    _say(f"free-running {name} B={inst.B} N={inst.N} K={inst.dense_k} R={inst.R} T={T}")
-    s = esp.Solver(inst)
+    _say(f"free-running {name} mode={mode} B={inst.B} N={inst.N} K={inst.dense_k} R={inst.R} T={T}")
+    s = esp.Solver(inst, mode=MODES[mode])
     g = s.solve(s.prices(inst.lam0), T, trace=True, trace_choice=True)
     torch.cuda.synchronize()
     ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
@@ -102,14 +106,14 @@ def test_granular_equals_fused(name):
 
 
 def test_run_to_run_and_geometry_determinism():
-    """Same inputs, different workgroup counts: bitwise identical results
-    (integer demand sums do not depend on the reduction tree)."""
+    """Same inputs, different workgroup counts and loop drivers: bitwise
+    identical results (integer demand sums do not depend on the tree)."""
     inst = workloads.make("large", n_jobs=6000)
     T = 40
     _say("determinism large_6000")
     outs = []
-    for nb in (0, 0, 1, 3, 64):
-        s = esp.Solver(inst, blocks_per_cluster=nb)
+    for nb, mode in ((0, 1), (0, 1), (1, 1), (3, 1), (64, 1), (0, 2), (1, 2), (3, 2), (64, 2), (0, 2)):
+        s = esp.Solver(inst, blocks_per_cluster=nb, mode=mode)
         g = s.solve(s.prices(inst.lam0), T, trace=True)
         torch.cuda.synchronize()
         outs.append((g["tr_lam"].cpu().numpy(), g["tr_U"].cpu().numpy(), g["choice"].cpu().numpy()))
@@ -119,10 +123,11 @@ def test_run_to_run_and_geometry_determinism():
             assert np.array_equal(a, b)
 
 
-def test_warm_start_continues_bitwise():
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_warm_start_continues_bitwise(mode):
     inst = workloads.make("small")
-    _say("warm start small")
-    s = esp.Solver(inst)
+    _say(f"warm start small {mode}")
+    s = esp.Solver(inst, mode=MODES[mode])
     full = s.solve(s.prices(inst.lam0), 90, trace=True)
     lam = s.prices(inst.lam0)
     a = s.solve(lam, 40, trace=True)
@@ -132,12 +137,13 @@ def test_warm_start_continues_bitwise():
     assert torch.equal(b["choice"], full["choice"])
 
 
-def test_early_stop_matches_oracle():
+@pytest.mark.parametrize("mode", sorted(MODES))
+def test_early_stop_matches_oracle(mode):
     inst = workloads.random_small(18, 10, 4, 2, dense=True, iters=500, eta0=0.02)
-    _say("early stop")
+    _say(f"early stop {mode}")
     tol = 1e-3
     ref = oracle.Oracle(inst).solve(tol=tol, trace_choice=True)
-    s = esp.Solver(inst)
+    s = esp.Solver(inst, mode=MODES[mode])
     g = s.solve(s.prices(inst.lam0), inst.iters, tol=tol, trace=True, trace_choice=True)
     torch.cuda.synchronize()
     n = int(ref["iters_done"][0])
