@@ -40,7 +40,8 @@ class _Problem(C.Structure):
         ("B", C.c_int32), ("N", C.c_int32), ("R", C.c_int32), ("nnz", C.c_int64),
         ("offsets", C.c_void_p), ("utility", C.c_void_p), ("demand", C.c_void_p),
         ("feasible", C.c_void_p), ("capacity", C.c_void_p), ("eta0", C.c_void_p),
-        ("rule", C.c_int32),
+        ("rule", C.c_int32), ("current", C.c_void_p), ("switch_cost", C.c_void_p),
+        ("penalty", C.c_void_p),
     ]
 
 
@@ -66,7 +67,7 @@ def _declare(L):
     vp, i32, i64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_double
     L.orc_exact_sum_f32.argtypes = [vp, i64]
     L.orc_exact_sum_f32.restype = dbl
-    L.orc_score.argtypes = [vp, C.c_int, i64, vp]
+    L.orc_score.argtypes = [vp, C.c_int, i64, i32, vp]
     L.orc_score.restype = dbl
     L.orc_select.argtypes = [vp, C.c_int, vp, vp]
     L.orc_select.restype = None
@@ -122,15 +123,22 @@ class Oracle:
                          else np.ascontiguousarray(inst.feasible, dtype=np.uint8))
         self.B, self.N, self.R = self.utility.shape[0], self.offsets.size - 1, self.demand.shape[2]
         self.rule = int(inst.rule)
+        cur = getattr(inst, "current", None)
+        pen = getattr(inst, "penalty", None)
+        self.current = None if cur is None else np.ascontiguousarray(cur, dtype=np.int32)
+        self.switch_cost = (None if cur is None else
+                            np.ascontiguousarray(getattr(inst, "switch_cost"), dtype=np.float64))
+        self.penalty = None if pen is None else np.ascontiguousarray(pen, dtype=np.float32)
         self._prob = _Problem(self.B, self.N, self.R, int(self.offsets[-1]),
                               _p(self.offsets), _p(self.utility), _p(self.demand),
-                              _p(self.feasible), _p(self.capacity), _p(self.eta0), self.rule)
+                              _p(self.feasible), _p(self.capacity), _p(self.eta0), self.rule,
+                              _p(self.current), _p(self.switch_cost), _p(self.penalty))
         self._pp = C.addressof(self._prob)
 
     # single steps -------------------------------------------------------
-    def score(self, b: int, e: int, lam) -> float:
+    def score(self, b: int, j: int, k: int, lam) -> float:
         lam = np.ascontiguousarray(lam, dtype=np.float64)
-        return float(self.L.orc_score(self._pp, b, e, _p(lam)))
+        return float(self.L.orc_score(self._pp, b, j, k, _p(lam)))
 
     def select(self, b: int, lam) -> np.ndarray:
         lam = np.ascontiguousarray(lam, dtype=np.float64)

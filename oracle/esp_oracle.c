@@ -15,6 +15,10 @@
  *     Eq. 6): for fixed prices lambda, job j picks
  *         c_j = argmax_k [ u_jk - sum_r lambda_r d_jkr ]
  *     by enumerating its family, lowest index winning ties;
+ *   - optionally with the penalty Gamma_j(k) of the ESP score (Eq. 7,
+ *     Sec. 3.2.3), subtracted after the rent: a switching cost gamma_0 for
+ *     every configuration other than the job's current one, and a given
+ *     interference penalty per configuration;
  *   - the aggregate demand U_r = sum_j d_{j,c_j,r} of the current selection
  *     (Sec. 3.2.3, definition under Eq. 8), as the exact real sum rounded once
  *     to binary64 (round-to-nearest-even);
@@ -28,7 +32,9 @@
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   score    rent = d0*l0; rent = rent + d_r*l_r (r = 1..R-1); s = u - rent,
- *            table values widened exactly from fp32 to fp64;
+ *            table values widened exactly from fp32 to fp64; with Eq. 7's
+ *            penalty: s = s - gamma_0 (k != current, current >= 0), then
+ *            s = s - penalty_jk;
  *   ties     the lowest configuration index wins (strict '>' scan);
  *   t        1-based within one solve; a warm start passes t_start;
  *   project  x > 0 ? x : +0.0 (a stored price is never -0.0);
@@ -124,14 +130,37 @@ double orc_exact_sum_f32(const float *v, int64_t n)
 static const float *util_of(const orc_problem *p, int b) { return p->utility + (int64_t)b * p->nnz; }
 static const float *dem_of(const orc_problem *p, int b) { return p->demand + (int64_t)b * p->nnz * p->R; }
 
-/* Score of table entry e at prices lam (Sec. 3.2.2, the bracket of Eq. 6). */
-double orc_score(const orc_problem *p, int b, int64_t e, const double *lam)
+/* Score of configuration k of job j at prices lam (Sec. 3.2.2, the bracket
+ * of Eq. 6), minus the penalty Gamma of Eq. 7 when one is given. */
+double orc_score(const orc_problem *p, int b, int64_t j, int32_t k, const double *lam)
 {
+    const int64_t e = p->offsets[j] + k;
     const float *d = dem_of(p, b) + e * p->R;
     double rent = (double)d[0] * lam[0];
+    double s;
     int r;
     for (r = 1; r < p->R; r++) rent = rent + (double)d[r] * lam[r];
-    return (double)util_of(p, b)[e] - rent;
+    s = (double)util_of(p, b)[e] - rent;
+    if (p->current != NULL) {
+        const int32_t cur = p->current[(int64_t)b * p->N + j];
+        if (cur >= 0 && k != cur) s = s - p->switch_cost[b];
+    }
+    if (p->penalty != NULL) s = s - (double)p->penalty[(int64_t)b * p->nnz + e];
+    return s;
+}
+
+/* The objective each job maximises at zero prices (Eq. 1 with Eq. 7's penalty):
+ * u_jk - gamma_0 [k != current] - penalty_jk. */
+static double penalized_utility(const orc_problem *p, int b, int64_t j, int32_t k)
+{
+    const int64_t e = p->offsets[j] + k;
+    double v = (double)util_of(p, b)[e];
+    if (p->current != NULL) {
+        const int32_t cur = p->current[(int64_t)b * p->N + j];
+        if (cur >= 0 && k != cur) v = v - p->switch_cost[b];
+    }
+    if (p->penalty != NULL) v = v - (double)p->penalty[(int64_t)b * p->nnz + e];
+    return v;
 }
 
 static int entry_allowed(const orc_problem *p, int b, int64_t e)
@@ -150,7 +179,7 @@ void orc_select(const orc_problem *p, int b, const double *lam, int32_t *choice)
         for (e = lo; e < hi; e++) {
             double s;
             if (!entry_allowed(p, b, e)) continue;
-            s = orc_score(p, b, e, lam);
+            s = orc_score(p, b, j, (int32_t)(e - lo), lam);
             if (best_k < 0 || s > best) { best = s; best_k = (int32_t)(e - lo); }
         }
         choice[j] = best_k;                 /* -1 only for a family with no allowed entry */
@@ -199,18 +228,19 @@ double orc_dual_value(const orc_problem *p, int b, const double *lam, const int3
     int64_t j;
     int r;
     for (j = 0; j < p->N; j++)
-        if (choice[j] >= 0) v = v + orc_score(p, b, p->offsets[j] + choice[j], lam);
+        if (choice[j] >= 0) v = v + orc_score(p, b, j, choice[j], lam);
     for (r = 0; r < p->R; r++) v = v + lam[r] * p->capacity[(int64_t)b * p->R + r];
     return v;
 }
 
-/* Objective of Eq. 1 at the selection: sum_j u_{j,c_j}. */
+/* Objective of Eq. 1 at the selection: sum_j u_{j,c_j} (less Eq. 7's penalty
+ * when one is given). */
 double orc_primal_value(const orc_problem *p, int b, const int32_t *choice)
 {
     double v = 0.0;
     int64_t j;
     for (j = 0; j < p->N; j++)
-        if (choice[j] >= 0) v = v + (double)util_of(p, b)[p->offsets[j] + choice[j]];
+        if (choice[j] >= 0) v = v + penalized_utility(p, b, j, choice[j]);
     return v;
 }
 

@@ -22,10 +22,14 @@ typedef struct {
     const double *capacity;   /* [B][R] */
     const double *eta0;       /* [B] */
     int32_t rule;
+    /* Penalty term Gamma of Eq. 7 (all optional, NULL = absent): */
+    const int32_t *current;   /* [B][N] current configuration, -1 = none */
+    const double *switch_cost;/* [B] gamma_0, paid by every k != current */
+    const float *penalty;     /* [B][nnz] interference penalty per configuration */
 } orc_problem;
 
 double orc_exact_sum_f32(const float *v, int64_t n);
-double orc_score(const orc_problem *p, int b, int64_t e, const double *lam);
+double orc_score(const orc_problem *p, int b, int64_t j, int32_t k, const double *lam);
 void orc_select(const orc_problem *p, int b, const double *lam, int32_t *choice);
 void orc_demand(const orc_problem *p, int b, const int32_t *choice, double *U);
 double orc_eta(int rule, double eta0, int64_t t);

@@ -47,18 +47,38 @@ def golden_instance(g: dict) -> workloads.Instance:
     cap = np.array(g["capacity"], dtype=np.float64).reshape(1, R)
     rule = workloads.STEP_CONST if g["rule"] == ["const"] else workloads.STEP_INV_SQRT
     lam0 = np.array(g.get("lam0", [0.0] * R), dtype=np.float64).reshape(1, R)
-    return workloads.Instance("golden", 0, offsets, util, dem, cap,
+    inst = workloads.Instance("golden", 0, offsets, util, dem, cap,
                               np.array(g["eta0"], dtype=np.float64), rule, lam0, int(g["iters"][0]))
+    if "current" in g:
+        inst.current = np.array(g["current"], dtype=np.int32).reshape(1, -1)
+        inst.switch_cost = np.array(g["switch_cost"], dtype=np.float64)
+    if "penalty" in g:
+        inst.penalty = np.array(g["penalty"], dtype=np.float32).reshape(1, nnz)
+    return inst
+
+
+def penalized_utility(inst, b, j, k) -> Fraction:
+    """u_jk less the penalty of Eq. 7 (switching cost, interference), exactly."""
+    e = int(inst.offsets[j]) + k
+    v = Fraction(float(inst.utility[b, e]))
+    cur = getattr(inst, "current", None)
+    if cur is not None and cur[b, j] >= 0 and k != cur[b, j]:
+        v -= Fraction(float(inst.switch_cost[b]))
+    pen = getattr(inst, "penalty", None)
+    if pen is not None:
+        v -= Fraction(float(pen[b, e]))
+    return v
 
 
 def brute_force_optimum(inst: workloads.Instance, b: int = 0):
-    """max sum_j u_{j,c_j} over all selections with sum_j d_{j,c_j} <= C
-    (Eq. 1-3), in exact rational arithmetic.  Returns (P*, argmax tuple) or
-    (None, None) when no selection is feasible."""
+    """max sum_j u_{j,c_j} (less Eq. 7's penalty when given) over all
+    selections with sum_j d_{j,c_j} <= C (Eq. 1-3), in exact rational
+    arithmetic.  Returns (P*, argmax tuple) or (None, None) when no selection
+    is feasible."""
     off = inst.offsets
     N, R = inst.N, inst.R
     fam = [range(int(off[j + 1] - off[j])) for j in range(N)]
-    u = [[Fraction(float(inst.utility[b, off[j] + k])) for k in fam[j]] for j in range(N)]
+    u = [[penalized_utility(inst, b, j, k) for k in fam[j]] for j in range(N)]
     d = [[[Fraction(float(inst.demand[b, off[j] + k, r])) for r in range(R)] for k in fam[j]]
          for j in range(N)]
     cap = [Fraction(float(c)) for c in inst.capacity[b]]
@@ -86,7 +106,8 @@ def lp_optimum(inst: workloads.Instance, b: int = 0) -> float:
     from scipy.optimize import linprog
     off = inst.offsets
     N, R, nnz = inst.N, inst.R, inst.nnz
-    c = -inst.utility[b].astype(np.float64)
+    c = -np.array([float(penalized_utility(inst, b, j, k)) for j in range(N)
+                   for k in range(int(off[j + 1] - off[j]))])
     A_eq = np.zeros((N, nnz))
     for j in range(N):
         A_eq[j, off[j]:off[j + 1]] = 1.0
@@ -99,8 +120,11 @@ def lp_optimum(inst: workloads.Instance, b: int = 0) -> float:
     return float("nan") if res.status == 2 else -float(res.fun)
 
 
-def exact_score(inst, b, e, lam) -> Fraction:
-    s = Fraction(float(inst.utility[b, e]))
+def exact_score(inst, b, e, lam, j=None) -> Fraction:
+    """Exact rational score of entry e (job j), penalties included."""
+    if j is None:
+        j = int(np.searchsorted(inst.offsets, e, side="right") - 1)
+    s = penalized_utility(inst, b, j, e - int(inst.offsets[j]))
     for r in range(inst.R):
         s -= Fraction(float(lam[r])) * Fraction(float(inst.demand[b, e, r]))
     return s

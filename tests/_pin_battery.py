@@ -17,7 +17,7 @@ from tests._helpers import exact_score, golden_instance, lp_optimum, read_golden
 
 def battery(L) -> None:
     # hand-derived traces (Sec. 3.2.2 argmax, Eq. 8 update)
-    for name in ("hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt"):
+    for name in ("hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt", "hand_penalty.txt"):
         g = read_golden(name)
         res = oracle.Oracle(golden_instance(g), L).solve(trace_choice=True)
         for i, row in enumerate(g["trace"]):
@@ -38,9 +38,12 @@ def battery(L) -> None:
         assert oracle.exact_sum_f32(v, L) == math.fsum(float(x) for x in v)
     assert oracle.exact_sum_f32(np.array([2.0 ** 53, 1.0], np.float32), L) == 2.0 ** 53
     assert oracle.exact_sum_f32(np.array([2.0 ** 53, 2.0, 1.0], np.float32), L) == 2.0 ** 53 + 4
-    # exact per-job optimality and LP weak duality on random instances
-    for seed in (3, 4):
+    # exact per-job optimality and LP weak duality on random instances,
+    # without and with the penalty of Eq. 7
+    for seed in (3, 4, 5):
         inst = workloads.random_small(seed, 6, 5, 3, iters=40, eta0=0.1)
+        if seed == 5:
+            workloads.with_penalties(inst, seed)
         res = oracle.Oracle(inst, L).solve(trace_choice=True)
         lams = np.concatenate([inst.lam0, res["tr_lam"][:-1, 0]], axis=0)
         LP = lp_optimum(inst)

@@ -18,7 +18,7 @@ def _bits(x: float) -> int:
     return struct.unpack("<Q", struct.pack("<d", x))[0]
 
 
-@pytest.mark.parametrize("name", ["hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt"])
+@pytest.mark.parametrize("name", ["hand_r1_tie.txt", "hand_r2.txt", "hand_projection.txt", "hand_penalty.txt"])
 def test_hand_trace(name):
     g = read_golden(name)
     inst = golden_instance(g)

@@ -16,7 +16,14 @@ SRC = os.path.join(ROOT, "oracle", "esp_oracle.c")
 MUTANTS = {
     "rent_drops_a_term": ("for (r = 1; r < p->R; r++) rent", "for (r = 2; r < p->R; r++) rent"),
     "rent_wrong_price": ("rent = rent + (double)d[r] * lam[r];", "rent = rent + (double)d[r] * lam[0];"),
-    "score_sign": ("return (double)util_of(p, b)[e] - rent;", "return (double)util_of(p, b)[e] + rent;"),
+    "score_sign": ("s = (double)util_of(p, b)[e] - rent;", "s = (double)util_of(p, b)[e] + rent;"),
+    "switch_sign": ("if (cur >= 0 && k != cur) s = s - p->switch_cost[b];",
+                    "if (cur >= 0 && k != cur) s = s + p->switch_cost[b];"),
+    "switch_on_current": ("if (cur >= 0 && k != cur) s = s - p->switch_cost[b];",
+                          "if (cur >= 0 && k == cur) s = s - p->switch_cost[b];"),
+    "penalty_dropped": ("if (p->penalty != NULL) s = s - (double)p->penalty[(int64_t)b * p->nnz + e];", ";"),
+    "penalty_wrong_entry": ("if (p->penalty != NULL) s = s - (double)p->penalty[(int64_t)b * p->nnz + e];",
+                            "if (p->penalty != NULL) s = s - (double)p->penalty[(int64_t)b * p->nnz + p->offsets[j]];"),
     "ties_to_highest": ("if (best_k < 0 || s > best)", "if (best_k < 0 || s >= best)"),
     "update_sign": ("double g = U[r] - C[r];", "double g = C[r] - U[r];"),
     "no_projection": ("lam[r] = (x > 0.0) ? x : 0.0;", "lam[r] = x;"),

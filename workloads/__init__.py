@@ -30,7 +30,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = [
-    "Instance", "make", "NAMES", "random_small", "uniform_offsets",
+    "Instance", "make", "NAMES", "random_small", "uniform_offsets", "with_penalties",
     "STEP_CONST", "STEP_INV_SQRT",
 ]
 
@@ -78,6 +78,7 @@ def _normal(seed: int, stream: int, idx: np.ndarray) -> np.ndarray:
 _S_B, _S_M, _S_S, _S_F, _S_P, _S_Q, _S_CPU, _S_IO = 10, 12, 13, 14, 15, 16, 17, 18
 _S_K, _S_TYPE, _S_OFF, _S_STRIDE, _S_BINF, _S_BSAT, _S_W, _S_KV = 20, 21, 22, 23, 24, 25, 26, 27
 _S_G, _S_ETA, _S_TINY_U, _S_TINY_D, _S_TINY_K, _S_TINY_C = 30, 31, 40, 41, 42, 43
+_S_CUR, _S_PEN = 50, 52
 
 
 @dataclasses.dataclass
@@ -105,6 +106,10 @@ class Instance:
     iters: int
     feasible: Optional[np.ndarray] = None      # uint8 [B, nnz] (Eq. 4 mask) or None
     dense_k: Optional[int] = None              # K when every family has K configs
+    # Penalty Gamma of the ESP score (Eq. 7), optional:
+    current: Optional[np.ndarray] = None       # int32 [B, N] current configuration, -1 = none
+    switch_cost: Optional[np.ndarray] = None   # float64 [B] switching cost gamma_0
+    penalty: Optional[np.ndarray] = None       # float32 [B, nnz] interference penalty
 
     @property
     def B(self) -> int:
@@ -131,8 +136,9 @@ class Instance:
         h = hashlib.sha256()
         for a in (self.offsets, self.utility, self.demand, self.capacity, self.eta0, self.lam0):
             h.update(np.ascontiguousarray(a).tobytes())
-        if self.feasible is not None:
-            h.update(np.ascontiguousarray(self.feasible).tobytes())
+        for extra in (self.feasible, self.current, self.switch_cost, self.penalty):
+            if extra is not None:
+                h.update(np.ascontiguousarray(extra).tobytes())
         h.update(f"{self.rule}:{self.iters}".encode())
         return h.hexdigest()
 
@@ -370,6 +376,26 @@ def make(name: str, **kw) -> Instance:
 # ---------------------------------------------------------------------------
 # Small random instances for brute force / property tests
 # ---------------------------------------------------------------------------
+
+def with_penalties(inst: Instance, seed: int, switch_cost: float = 0.05, penalty_scale: float = 0.2,
+                   frac_current: float = 0.8, dyadic: bool = False) -> Instance:
+    """Attach Eq. 7 penalty inputs to an instance: a current configuration for
+    a fraction of the jobs (-1 for the rest), a switching cost per cluster and
+    an interference penalty U[0, penalty_scale) per configuration (multiples
+    of 1/64 when ``dyadic``).  Returns the same instance, modified."""
+    B, N, nnz = inst.B, inst.N, inst.nnz
+    j = np.arange(B * N, dtype=np.int64)
+    sizes = np.tile(np.diff(inst.offsets), B)
+    cur = np.floor(_uniform(seed, _S_CUR, j) * sizes).astype(np.int64)
+    cur = np.where(_uniform(seed, _S_CUR + 1, j) < frac_current, cur, -1)
+    inst.current = cur.reshape(B, N).astype(np.int32)
+    inst.switch_cost = np.full(B, float(switch_cost))
+    pen = penalty_scale * _uniform(seed, _S_PEN, np.arange(B * nnz, dtype=np.int64))
+    if dyadic:
+        pen = np.floor(pen * 64.0) / 64.0
+    inst.penalty = _f32(pen).reshape(B, nnz)
+    return inst
+
 
 def random_small(seed: int, n_jobs: int, max_k: int, n_res: int, *, dense: bool = False,
                  dyadic: bool = False, n_clusters: int = 1, eta0: float = 0.05,
