@@ -88,6 +88,13 @@ typedef struct {
     const double *capacity;          /* [B][R]: C_r (or C_eff of Eq. 12); finite, |C_r| <= 2^200 */
     const uint8_t *feasible;         /* optional [B][nnz]: 0 marks a configuration that violates the
                                         performance floor of Eq. 4 (never selected); NULL = all allowed */
+    /* Optional penalty Gamma_j(c) of the ESP score (Eq. 7), subtracted after
+     * the rent: s = (u - rent) - gamma_0 [k != current_j] - penalty_jk.
+     * Give current + switch_cost, penalty, or both; all NULL = no penalty
+     * (then esp_set_penalties cannot be used on the context). */
+    const int32_t *current;          /* [B][N]: the job's current configuration index, -1 = none */
+    const double *switch_cost;       /* [B]: gamma_0, finite, 0 <= gamma_0 <= 2^100 (with current) */
+    const float *penalty;            /* [B][nnz]: interference penalty, finite and >= 0 */
 } esp_problem;
 
 typedef struct {
@@ -187,6 +194,20 @@ esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_star
  * a choice index outside its family; ESP_OK otherwise.
  */
 esp_status esp_device_status(esp_ctx *ctx, void *stream);
+
+/*
+ * esp_set_penalties (Eq. 7): replace the penalty inputs of a context that was
+ * created with them (e.g. between the ESP-IAC rounds of Alg. 1).  Same
+ * meaning and layout as the esp_problem fields (host pointers; current and
+ * switch_cost may be NULL for "no switching cost", penalty NULL for zero
+ * penalties).  Stream-ordered after earlier work on `stream`; host arrays may
+ * be freed when the call returns.
+ * Errors: ESP_ERR_STATE (NULL context, or one created without penalties),
+ * ESP_ERR_INVALID_ARG (current out of range, negative penalty or switching
+ * cost), ESP_ERR_NONFINITE, ESP_ERR_RANGE, ESP_ERR_DEVICE.
+ */
+esp_status esp_set_penalties(esp_ctx *ctx, const int32_t *current, const double *switch_cost, const float *penalty,
+                             void *stream);
 
 /* esp_destroy: free the host-side context (the workspace stays the caller's).
  * Waits for nothing: the caller must not destroy a context with work in flight. */

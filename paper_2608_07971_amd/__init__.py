@@ -48,6 +48,7 @@ class esp_problem(C.Structure):
         ("num_clusters", C.c_int32), ("num_jobs", C.c_int32), ("num_resources", C.c_int32),
         ("configs_per_job", C.c_int32), ("family_offsets", C.c_void_p), ("utility", C.c_void_p),
         ("demand", C.c_void_p), ("capacity", C.c_void_p), ("feasible", C.c_void_p),
+        ("current", C.c_void_p), ("switch_cost", C.c_void_p), ("penalty", C.c_void_p),
     ]
 
 
@@ -76,6 +77,7 @@ _SIGS = {
     "esp_update_prices": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p], C.c_int),
     "esp_solve": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_void_p,
                    C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_set_penalties": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
     "esp_destroy": ([C.c_void_p], C.c_int),
     "esp_status_string": ([C.c_int], C.c_char_p),
@@ -132,7 +134,11 @@ def _ptr(t) -> Optional[int]:
 class Problem:
     """Host arrays of an esp_problem kept alive for the duration of a call."""
 
-    def __init__(self, offsets, utility, demand, capacity, feasible=None, dense_k: Optional[int] = None):
+    def __init__(self, offsets, utility, demand, capacity, feasible=None, dense_k: Optional[int] = None,
+                 current=None, switch_cost=None, penalty=None):
+        self.current = None if current is None else np.ascontiguousarray(current, dtype=np.int32)
+        self.switch_cost = None if switch_cost is None else np.ascontiguousarray(switch_cost, dtype=np.float64)
+        self.penalty = None if penalty is None else np.ascontiguousarray(penalty, dtype=np.float32)
         self.utility = np.ascontiguousarray(utility, dtype=np.float32)
         self.demand = np.ascontiguousarray(demand, dtype=np.float32)
         self.capacity = np.ascontiguousarray(capacity, dtype=np.float64)
@@ -145,12 +151,18 @@ class Problem:
         self.c = esp_problem(B, N, R, int(dense_k or 0),
                              None if self.offsets is None else self.offsets.ctypes.data,
                              self.utility.ctypes.data, self.demand.ctypes.data, self.capacity.ctypes.data,
-                             None if self.feasible is None else self.feasible.ctypes.data)
+                             None if self.feasible is None else self.feasible.ctypes.data,
+                             _np_ptr(self.current), _np_ptr(self.switch_cost), _np_ptr(self.penalty))
 
     @classmethod
     def from_instance(cls, inst) -> "Problem":
         return cls(inst.offsets, inst.utility, inst.demand, inst.capacity, inst.feasible,
-                   dense_k=getattr(inst, "dense_k", None))
+                   dense_k=getattr(inst, "dense_k", None), current=getattr(inst, "current", None),
+                   switch_cost=getattr(inst, "switch_cost", None), penalty=getattr(inst, "penalty", None))
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data
 
 
 def esp_workspace_size(problem: Problem, options: Optional[esp_options] = None) -> int:
@@ -190,6 +202,14 @@ def esp_solve(ctx: int, prices, iters: int, t_start: int = 1, tol: float = 0.0, 
     _check(lib().esp_solve(ctx, _ptr(prices), int(iters), int(t_start), float(tol), _ptr(choice), _ptr(demand),
                            None if trace is None else C.addressof(trace), _ptr(iters_done), _stream(stream)),
            "esp_solve")
+
+
+def esp_set_penalties(ctx: int, current=None, switch_cost=None, penalty=None, stream=None) -> None:
+    cur = None if current is None else np.ascontiguousarray(current, dtype=np.int32)
+    swc = None if switch_cost is None else np.ascontiguousarray(switch_cost, dtype=np.float64)
+    pen = None if penalty is None else np.ascontiguousarray(penalty, dtype=np.float32)
+    _check(lib().esp_set_penalties(ctx, _np_ptr(cur), _np_ptr(swc), _np_ptr(pen), _stream(stream)),
+           "esp_set_penalties")
 
 
 def esp_device_status(ctx: int, stream=None) -> int:
@@ -272,6 +292,9 @@ class Solver:
         esp_solve(self.ctx, prices, iters, t_start, tol, out["choice"], out["U"], tr, out["iters_done"], stream)
         out["lam"] = prices
         return out
+
+    def set_penalties(self, current=None, switch_cost=None, penalty=None, stream=None) -> None:
+        esp_set_penalties(self.ctx, current, switch_cost, penalty, stream)
 
     def device_status(self, stream=None) -> int:
         return esp_device_status(self.ctx, stream)

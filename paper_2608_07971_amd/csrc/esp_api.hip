@@ -31,13 +31,15 @@ struct Plan {
     int K = 0;          // dense family size handled by the dense kernel, else 0
     int lpj = 0;        // lanes per job of the dense kernel
     bool csr = false;
+    bool pen = false;   // a penalty column follows the demand columns
     int64_t nnz = 0;
     int tiles = 0;      // per cluster
     size_t col_len = 0; // floats per column
     int nblk = 0;       // workgroups per cluster
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_status = 0, total = 0;
+           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, total = 0;
+    size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
 // Compute units of the current device (256 on MI355X); 256 when no device
@@ -97,6 +99,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->B = p->num_clusters;
     pl->N = p->num_jobs;
     pl->R = p->num_resources;
+    pl->pen = p->current != nullptr || p->penalty != nullptr;
     if (uk > 0 && dense_fast_k(uk)) {
         pl->K = uk;
         pl->lpj = uk / 4;
@@ -134,7 +137,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
 
     const size_t B = pl->B, R = pl->R;
     size_t o = 0;
-    pl->o_table = o; o = align_up(o + B * (R + 1) * pl->col_len * sizeof(float));
+    pl->o_table = o; o = align_up(o + B * pl->columns() * pl->col_len * sizeof(float));
     pl->o_meta = o;  o = align_up(o + (pl->csr ? static_cast<size_t>(pl->tiles) * sizeof(TileMeta) : 0));
     pl->o_jobs = o;  o = align_up(o + (pl->csr ? static_cast<size_t>(pl->N) * sizeof(JobSlot) : 0));
     pl->o_shift = o; o = align_up(o + B * R * sizeof(int32_t));
@@ -145,6 +148,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
     pl->o_iters = o; o = align_up(o + B * sizeof(int32_t));
     pl->o_epoch = o; o = align_up(o + B * sizeof(uint32_t));
+    pl->o_swc = o;   o = align_up(o + B * sizeof(double));
     pl->o_status = o; o = align_up(o + sizeof(int32_t));
     pl->total = o;
     return ESP_OK;
@@ -188,10 +192,54 @@ struct esp_ctx {
     bool eta_pending = false;
     int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
     int mode = ESP_MODE_AUTO;
+    std::vector<int64_t> off;          // family offsets (host copy)
+    std::vector<int64_t> slot_of;      // first table slot of each family
     KArgs base{};
 };
 
 namespace {
+
+// Validate the penalty inputs of Eq. 7 against the family layout.
+esp_status validate_penalties(int B, int N, int64_t nnz, const std::vector<int64_t> &off, const int32_t *current,
+                              const double *switch_cost, const float *penalty) {
+    if ((current == nullptr) != (switch_cost == nullptr)) return ESP_ERR_INVALID_ARG;
+    if (current) {
+        for (int b = 0; b < B; ++b) {
+            const double g = switch_cost[b];
+            if (!std::isfinite(g)) return ESP_ERR_NONFINITE;
+            if (!(g >= 0.0)) return ESP_ERR_INVALID_ARG;
+            if (g > 0x1p100) return ESP_ERR_RANGE;
+            for (int j = 0; j < N; ++j) {
+                const int32_t c = current[static_cast<size_t>(b) * N + j];
+                if (c < -1 || c >= off[j + 1] - off[j]) return ESP_ERR_INVALID_ARG;
+            }
+        }
+    }
+    if (penalty) {
+        for (size_t e = 0; e < static_cast<size_t>(B) * nnz; ++e) {
+            const float v = penalty[e];
+            if (!std::isfinite(v)) return ESP_ERR_NONFINITE;
+            if (v < 0.0f) return ESP_ERR_INVALID_ARG;
+        }
+    }
+    return ESP_OK;
+}
+
+// Penalty column of cluster b into h (col_len floats): |penalty| with the sign
+// bit set on entries that pay the switching cost.
+void fill_penalty_column(float *h, size_t col_len, int b, int N, int64_t nnz, const std::vector<int64_t> &off,
+                         const std::vector<int64_t> &slot_of, const int32_t *current, const float *penalty) {
+    std::fill(h, h + col_len, 0.0f);
+    for (int j = 0; j < N; ++j) {
+        const int64_t k = off[j + 1] - off[j];
+        const int32_t cur = current ? current[static_cast<size_t>(b) * N + j] : -1;
+        for (int64_t i = 0; i < k; ++i) {
+            float v = penalty ? penalty[static_cast<size_t>(b) * nnz + off[j] + i] : 0.0f;
+            v = (v == 0.0f) ? 0.0f : v;                 // +0.0 for either zero
+            h[slot_of[j] + i] = (cur >= 0 && i != cur) ? -v : v;   // -0.0 when the penalty is zero
+        }
+    }
+}
 
 esp_status check_ctx(const esp_ctx *c) {
     return (c != nullptr && c->magic == kMagic) ? ESP_OK : ESP_ERR_STATE;
@@ -301,6 +349,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                 if (!any) return ESP_ERR_EMPTY_FAMILY;
             }
     }
+    if (pl.pen && (st = validate_penalties(B, N, nnz, off, p->current, p->switch_cost, p->penalty)) != ESP_OK)
+        return st;
     // Fixed-point window per (cluster, resource): lowest set bit over the
     // column.  The highest bit plus log2(N + 1) fixes the accumulator width:
     // 64-bit when it is at most 63 for every column, 128-bit when at most 127.
@@ -385,32 +435,37 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
         const float neg_inf = -__builtin_inff();
         const float pad_u = pl.csr ? neg_inf : 0.0f;
         int which = 0;
+        const int ncol = static_cast<int>(pl.columns());
         for (int b = 0; b < B; ++b) {
-            for (int a = 0; a <= R; ++a) {
+            for (int a = 0; a < ncol; ++a) {
                 if (pp.pending[which]) {
                     if (hipEventSynchronize(pp.ev[which]) != hipSuccess) return fail(ESP_ERR_DEVICE);
                     pp.pending[which] = false;
                 }
                 float *h = pp.buf[which];
-                std::fill(h, h + pl.col_len, a == 0 ? pad_u : 0.0f);
-                const float *u = p->utility + static_cast<size_t>(b) * nnz;
-                const float *d = p->demand + static_cast<size_t>(b) * nnz * R + (a - 1);
-                const uint8_t *f = p->feasible ? p->feasible + static_cast<size_t>(b) * nnz : nullptr;
-                for (int j = 0; j < N; ++j) {
-                    const int64_t e0 = off[j], k = off[j + 1] - off[j];
-                    float *dst = h + slot_of[j];
-                    if (a == 0) {
-                        for (int64_t i = 0; i < k; ++i)
-                            dst[i] = (f && f[e0 + i] == 0) ? neg_inf : u[e0 + i];
-                    } else {
-                        for (int64_t i = 0; i < k; ++i) {
-                            const float v = d[static_cast<size_t>(e0 + i) * R];
-                            dst[i] = (v == 0.0f) ? 0.0f : v;     // -0.0 -> +0.0
+                if (a == R + 1) {
+                    fill_penalty_column(h, pl.col_len, b, N, nnz, off, slot_of, p->current, p->penalty);
+                } else {
+                    std::fill(h, h + pl.col_len, a == 0 ? pad_u : 0.0f);
+                    const float *u = p->utility + static_cast<size_t>(b) * nnz;
+                    const float *d = p->demand + static_cast<size_t>(b) * nnz * R + (a - 1);
+                    const uint8_t *f = p->feasible ? p->feasible + static_cast<size_t>(b) * nnz : nullptr;
+                    for (int j = 0; j < N; ++j) {
+                        const int64_t e0 = off[j], k = off[j + 1] - off[j];
+                        float *dst = h + slot_of[j];
+                        if (a == 0) {
+                            for (int64_t i = 0; i < k; ++i)
+                                dst[i] = (f && f[e0 + i] == 0) ? neg_inf : u[e0 + i];
+                        } else {
+                            for (int64_t i = 0; i < k; ++i) {
+                                const float v = d[static_cast<size_t>(e0 + i) * R];
+                                dst[i] = (v == 0.0f) ? 0.0f : v;     // -0.0 -> +0.0
+                            }
                         }
                     }
                 }
                 float *dcol = reinterpret_cast<float *>(ws + pl.o_table) +
-                              (static_cast<size_t>(b) * (R + 1) + a) * pl.col_len;
+                              (static_cast<size_t>(b) * ncol + a) * pl.col_len;
                 if (hipMemcpyAsync(dcol, h, sizeof(float) * pl.col_len, hipMemcpyHostToDevice, s) != hipSuccess ||
                     hipEventRecord(pp.ev[which], s) != hipSuccess)
                     return fail(ESP_ERR_DEVICE);
@@ -419,6 +474,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
             }
         }
         std::vector<double> cap(p->capacity, p->capacity + static_cast<size_t>(B) * R);
+        std::vector<double> swc(B, 0.0);
+        if (p->switch_cost) swc.assign(p->switch_cost, p->switch_cost + B);
         bool ok = hipMemcpyAsync(ws + pl.o_shift, shift.data(), sizeof(int32_t) * shift.size(),
                                  hipMemcpyHostToDevice, s) == hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_cap, cap.data(), sizeof(double) * cap.size(), hipMemcpyHostToDevice, s) ==
@@ -427,6 +484,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_epoch, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
+                  hipMemcpyAsync(ws + pl.o_swc, swc.data(), sizeof(double) * B, hipMemcpyHostToDevice, s) ==
+                      hipSuccess &&
                   hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess;
         if (ok && pl.csr)
             ok = hipMemcpyAsync(ws + pl.o_meta, meta.data(), sizeof(TileMeta) * meta.size(), hipMemcpyHostToDevice,
@@ -437,9 +496,13 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
         pp.pending[0] = pp.pending[1] = false;
     }
 
+    c->off = std::move(off);
+    c->slot_of = std::move(slot_of);
     KArgs &k = c->base;
     k.table = reinterpret_cast<const float *>(ws + pl.o_table);
-    k.cluster_stride = static_cast<size_t>(R + 1) * pl.col_len;
+    k.cluster_stride = pl.columns() * pl.col_len;
+    k.has_pen = pl.pen ? 1 : 0;
+    k.switch_cost = reinterpret_cast<const double *>(ws + pl.o_swc);
     k.col_len = pl.col_len;
     k.meta = pl.csr ? reinterpret_cast<const TileMeta *>(ws + pl.o_meta) : nullptr;
     k.jobs = pl.csr ? reinterpret_cast<const JobSlot *>(ws + pl.o_jobs) : nullptr;
@@ -574,6 +637,35 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         hipMemcpyAsync(iters_done, d_iters, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s) != hipSuccess)
         return ESP_ERR_DEVICE;
     return ESP_OK;
+}
+
+esp_status esp_set_penalties(esp_ctx *c, const int32_t *current, const double *switch_cost, const float *penalty,
+                             void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (!c->pl.pen) return ESP_ERR_STATE;
+    const Plan &pl = c->pl;
+    if ((st = validate_penalties(pl.B, pl.N, pl.nnz, c->off, current, switch_cost, penalty)) != ESP_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    float *h = nullptr;
+    if (hipHostMalloc(reinterpret_cast<void **>(&h), sizeof(float) * pl.col_len) != hipSuccess) return ESP_ERR_DEVICE;
+    const size_t ncol = pl.columns();
+    for (int b = 0; b < pl.B && st == ESP_OK; ++b) {
+        // the previous copy out of h must be done before h is refilled
+        if (hipStreamSynchronize(s) != hipSuccess) { st = ESP_ERR_DEVICE; break; }
+        fill_penalty_column(h, pl.col_len, b, pl.N, pl.nnz, c->off, c->slot_of, current, penalty);
+        float *dcol = reinterpret_cast<float *>(c->ws + pl.o_table) + (static_cast<size_t>(b) * ncol + pl.R + 1) * pl.col_len;
+        if (hipMemcpyAsync(dcol, h, sizeof(float) * pl.col_len, hipMemcpyHostToDevice, s) != hipSuccess)
+            st = ESP_ERR_DEVICE;
+    }
+    std::vector<double> swc(pl.B, 0.0);
+    if (switch_cost) swc.assign(switch_cost, switch_cost + pl.B);
+    if (st == ESP_OK &&
+        (hipMemcpyAsync(c->ws + pl.o_swc, swc.data(), sizeof(double) * pl.B, hipMemcpyHostToDevice, s) != hipSuccess ||
+         hipStreamSynchronize(s) != hipSuccess))
+        st = ESP_ERR_DEVICE;
+    (void)hipHostFree(h);
+    return st;
 }
 
 esp_status esp_device_status(esp_ctx *c, void *stream) {

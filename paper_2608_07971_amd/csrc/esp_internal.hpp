@@ -83,6 +83,11 @@ struct KArgs {
     uint32_t *epoch;               // [B] (persistent launches)
     uint32_t epoch_base;           // epoch value when this launch starts
     int32_t sweep_alt;             // alternate the sweep direction between iterations
+    // Penalty of the ESP score (Eq. 7): column R + 1 of each cluster holds
+    // |penalty| per entry, its sign bit set when the entry is not the job's
+    // current configuration (the switching cost switch_cost[b] applies).
+    int32_t has_pen;
+    const double *switch_cost;     // [B]
 };
 
 constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound

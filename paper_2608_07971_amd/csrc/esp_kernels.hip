@@ -61,6 +61,14 @@ __device__ __forceinline__ void take_better(double &s, int &k, double os, int ok
     k = b ? ok : k;
 }
 
+// The penalty of the ESP score (Eq. 7) after the rent: the switching cost when
+// the stored penalty's sign bit marks "not the current configuration", then
+// the interference penalty |p|.
+__device__ __forceinline__ double penalize(double sc, float p, double sw) {
+    if (__float_as_uint(p) >> 31) sc = sc - sw;
+    return sc - static_cast<double>(fabsf(p));
+}
+
 // Argmax over aligned groups of LPJ lanes (LPJ in {1,2,4,8,16}); afterwards
 // every lane of a group holds the group's winner.
 template <int LPJ>
@@ -370,16 +378,18 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     // Tiles are swept front to back, or back to front when `rev` is set; the
     // exact demand sum does not depend on the order.
     const int last = a.tiles - 1;
-    auto load_tile = [&](int t, int rev, f4 &u, f4 (&d)[R]) {
+    const double sw = a.has_pen ? a.switch_cost[cl] : 0.0;
+    auto load_tile = [&](int t, int rev, f4 &u, f4 (&d)[R], f4 &pn) {
         const int tl = rev ? last - t : t;
         const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
         u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
         for (int r = 0; r < R; ++r)
             d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
+        if (a.has_pen) pn = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (R + 1) * a.col_len));
     };
     // Score, select and stage one tile held in registers.
-    auto process = [&](const KArgs &ai, int t, const f4 &u, const f4 (&d)[R]) {
+    auto process = [&](const KArgs &ai, int t, const f4 &u, const f4 (&d)[R], const f4 &pn) {
         const int tl = ai.reverse ? last - t : t;
         double best = 0.0;
         int bi = 0;
@@ -388,7 +398,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             double rent = static_cast<double>(d[0][i]) * lam[0];
 #pragma unroll
             for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
-            const double sc = static_cast<double>(u[i]) - rent;
+            double sc = static_cast<double>(u[i]) - rent;
+            if (a.has_pen) sc = penalize(sc, pn[i], sw);
             if (i == 0 || sc > best) { best = sc; bi = i; }
         }
         int k = gl * 4 + bi;
@@ -425,12 +436,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     // the loads of the next two are in flight (18 KB per wavefront at R = 8).
     // In a persistent launch the first two loads of the next iteration are
     // issued before the wait for its prices.
-    f4 ua, ub, uc;
+    f4 ua, ub, uc, pa = {}, pb = {}, pc = {};
     f4 da[R], db[R], dc[R];
     const int tile0 = blk * kBlockWaves + wave;
     auto prefetch_two = [&](int rev) {
-        if (tile0 < a.tiles) load_tile(tile0, rev, ua, da);
-        if (tile0 + stride < a.tiles) load_tile(tile0 + stride, rev, ub, db);
+        if (tile0 < a.tiles) load_tile(tile0, rev, ua, da, pa);
+        if (tile0 + stride < a.tiles) load_tile(tile0 + stride, rev, ub, db, pb);
     };
     prefetch_two(a.reverse);
     for (int it = 0; it < a.n_iters; ++it) {
@@ -438,12 +449,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         const int rev = ai.reverse;
         for (int tile = tile0; tile < a.tiles; tile += 3 * stride) {
             const int t1 = tile + stride, t2 = tile + 2 * stride;
-            if (t2 < a.tiles) load_tile(t2, rev, uc, dc);
-            process(ai, tile, ua, da);
-            if (t2 + stride < a.tiles) load_tile(t2 + stride, rev, ua, da);
-            if (t1 < a.tiles) process(ai, t1, ub, db);
-            if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, rev, ub, db);
-            if (t2 < a.tiles) process(ai, t2, uc, dc);
+            if (t2 < a.tiles) load_tile(t2, rev, uc, dc, pc);
+            process(ai, tile, ua, da, pa);
+            if (t2 + stride < a.tiles) load_tile(t2 + stride, rev, ua, da, pa);
+            if (t1 < a.tiles) process(ai, t1, ub, db, pb);
+            if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, rev, ub, db, pb);
+            if (t2 < a.tiles) process(ai, t2, uc, dc, pc);
         }
         if (!ai.reduce) return;
 
@@ -545,28 +556,31 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     const float *col = a.table + cl * a.cluster_stride;
     const size_t lane_off = static_cast<size_t>(lane) * 4;
     const int hshift = (lane & 7) * 4;                   // this lane's 4 head bits in its word
-    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R], uint32_t &hw) {
+    const double sw = a.has_pen ? a.switch_cost[cl] : 0.0;
+    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R], f4 &pn, uint32_t &hw) {
         const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
         u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
         for (int r = 0; r < R; ++r)
             d[r] = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (r + 1) * a.col_len));
+        if (a.has_pen) pn = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (R + 1) * a.col_len));
         hw = a.meta[tl].head[lane >> 3];
     };
     const int stride = a.nblk * kBlockWaves;
     const int last = a.tiles - 1;
     int tile = blk * kBlockWaves + wave;
-    f4 nu;
+    f4 nu, npn = {};
     f4 nd[R];
     uint32_t nhw = 0;
-    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd, nhw);
+    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd, npn, nhw);
     for (; tile < a.tiles; tile += stride) {
-        const f4 u = nu;
+        const f4 u = nu, pn = npn;
         f4 d[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) d[r] = nd[r];
         const uint32_t hbits = (nhw >> hshift) & 0xFu;
-        if (tile + stride < a.tiles) load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd, nhw);
+        if (tile + stride < a.tiles)
+            load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd, npn, nhw);
         const int tl = a.reverse ? last - tile : tile;
 
         double sc[4];
@@ -576,6 +590,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
 #pragma unroll
             for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
             sc[i] = static_cast<double>(u[i]) - rent;
+            if (a.has_pen) sc[i] = penalize(sc[i], pn[i], sw);
         }
         // Lane-local pass: the part before this lane's first head (it belongs to
         // a segment from lower lanes), segments complete inside the lane, and

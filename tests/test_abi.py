@@ -141,3 +141,27 @@ def test_null_context_is_rejected():
     assert L.esp_update_prices(None, None, 1, None, None) == esp.ESP_ERR_STATE
     assert L.esp_device_status(None, None) == esp.ESP_ERR_STATE
     assert L.esp_destroy(None) == esp.ESP_ERR_STATE
+
+
+def test_create_rejects_bad_penalties_on_host():
+    def mk():
+        return workloads.with_penalties(workloads.random_small(9, 8, 4, 3), 9)
+    neg = mk(); neg.penalty[0, 3] = -0.5
+    nan = mk(); nan.penalty[0, 3] = np.nan
+    cur = mk(); cur.current[0, 2] = 99
+    sw = mk(); sw.switch_cost[:] = -1.0
+    half = mk(); half.switch_cost = None
+    assert _create(neg)[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(nan)[0] == esp.ESP_ERR_NONFINITE
+    assert _create(cur)[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(sw)[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(half)[0] == esp.ESP_ERR_INVALID_ARG
+    assert _create(mk())[0] == esp.ESP_ERR_WORKSPACE         # valid problem, no workspace
+    assert esp.lib().esp_set_penalties(None, None, None, None, None) == esp.ESP_ERR_STATE
+
+
+def test_workspace_grows_by_one_column_with_penalties():
+    a = workloads.random_small(10, 50, 8, 3, dense=True)
+    b = workloads.with_penalties(workloads.random_small(10, 50, 8, 3, dense=True), 10)
+    na, nb = _ws(esp.Problem.from_instance(a)), _ws(esp.Problem.from_instance(b))
+    assert nb - na >= 50 * 8 * 4

@@ -288,3 +288,78 @@ def test_csr_mask_and_geometry():
         torch.cuda.synchronize()
         _check_trace(g, ref, inst.iters)
         s.close()
+
+
+# ---------------------------------------------------------------------------
+# Penalty Gamma of the ESP score (Eq. 7)
+# ---------------------------------------------------------------------------
+
+PEN_CASES = {
+    "dense_k64_r8": lambda: workloads.with_penalties(workloads.make("large", n_jobs=2051), 81, switch_cost=0.5),
+    "dense_batched": lambda: workloads.with_penalties(workloads.make("batched", n_jobs=300, n_clusters=3), 82),
+    "csr_ragged": lambda: workloads.with_penalties(workloads.make("ragged", n_jobs=9000), 83, switch_cost=0.2),
+    "switch_only": lambda: _switch_only(),
+    "penalty_only_dyadic": lambda: _penalty_only(),
+}
+
+
+def _switch_only():
+    inst = workloads.with_penalties(workloads.random_small(84, 900, 16, 3, dense=True, iters=80), 84)
+    inst.penalty = None
+    return inst
+
+
+def _penalty_only():
+    inst = workloads.random_small(85, 700, 12, 2, dyadic=True, iters=80, rule=workloads.STEP_CONST, eta0=0.125)
+    workloads.with_penalties(inst, 85, dyadic=True)
+    inst.current = None
+    inst.switch_cost = None
+    return inst
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
+@pytest.mark.parametrize("name", sorted(PEN_CASES))
+def test_penalty_trace_matches_oracle(name, mode):
+    inst = PEN_CASES[name]()
+    T = min(inst.iters, 80)
+    _say(f"penalty {name} mode={mode}")
+    s = esp.Solver(inst, mode=MODES[mode])
+    g = s.solve(s.prices(inst.lam0), T, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    ref = oracle.Oracle(inst).solve(iters=T, trace_choice=True)
+    _check_trace(g, ref, T)
+
+
+def test_hand_penalty_trace_on_gpu():
+    from tests._helpers import golden_instance, read_golden
+    g = read_golden("hand_penalty.txt")
+    inst = golden_instance(g)
+    _say("hand penalty trace")
+    s = esp.Solver(inst)
+    out = s.solve(s.prices(inst.lam0), inst.iters, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    for i, row in enumerate(g["trace"]):
+        assert list(out["tr_choice"][i, 0].cpu().numpy()) == [int(x) for x in row[2]]
+        assert np.array_equal(out["tr_lam"][i, 0].cpu().numpy(), np.array(row[4]))
+    assert list(out["choice"][0].cpu().numpy()) == [int(x) for x in g["final_choice"]]
+
+
+def test_set_penalties_between_rounds():
+    """Alg. 1 updates Gamma between ESP-IAC rounds: esp_set_penalties then a
+    warm-started solve equals the oracle on the updated problem."""
+    inst = workloads.with_penalties(workloads.make("large", n_jobs=1500), 86)
+    _say("set penalties")
+    s = esp.Solver(inst)
+    lam = s.prices(inst.lam0)
+    s.solve(lam, 20)
+    new = workloads.with_penalties(workloads.make("large", n_jobs=1500), 87, switch_cost=0.3)
+    s.set_penalties(new.current, new.switch_cost, new.penalty)
+    g = s.solve(lam, 25, t_start=21, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    ref1 = oracle.Oracle(inst).solve(iters=20)
+    ref2 = oracle.Oracle(new).solve(lam0=ref1["lam"], iters=25, t_start=21, trace_choice=True)
+    _check_trace(g, ref2, 25)
+    plain = esp.Solver(workloads.make("tiny"))
+    with pytest.raises(esp.EspError) as e:
+        plain.set_penalties(None, None, np.zeros((1, 512), np.float32))
+    assert e.value.code == esp.ESP_ERR_STATE
