@@ -37,6 +37,8 @@ def _parse():
     ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
     ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
     ap.add_argument("--mode", type=int, default=0, help="loop driver: 0 auto, 1 one launch per iteration, 2 persistent")
+    ap.add_argument("--penalties", action="store_true",
+                    help="add Eq. 7 penalty inputs (current configurations, switching cost, interference penalty)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -98,6 +100,8 @@ def main() -> int:
     t_gen = time.perf_counter()
     kw = {}
     inst = workloads.make(args.config, **kw)
+    if args.penalties:
+        workloads.with_penalties(inst, inst.seed + 100)
     T = args.iters or inst.iters
     print(f"[bench] {args.config}: B={inst.B} N={inst.N} R={inst.R} nnz={inst.nnz} T={T} "
           f"(generated in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
@@ -133,7 +137,8 @@ def main() -> int:
     # algorithmic bytes: the fp32 table read once per iteration, plus the
     # family boundaries (one 4-byte offset per job) for ragged families
     csr = inst.dense_k is None or inst.dense_k not in (4, 8, 16, 32, 64)
-    bytes_per_launch = configs * (1 + inst.R) * 4 + (4 * (inst.N + 1) if csr else 0)
+    pen_col = 1 if (inst.current is not None or inst.penalty is not None) else 0
+    bytes_per_launch = configs * (1 + inst.R + pen_col) * 4 + (4 * (inst.N + 1) if csr else 0)
     avg_launch_s = sec / launches
     achieved = bytes_per_launch / avg_launch_s / 1e9
     traffic = None

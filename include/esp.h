@@ -58,11 +58,11 @@ enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
 
 /* Loop drivers of esp_solve (results are identical in every mode). */
 enum {
-    ESP_MODE_AUTO = 0,        /* persistent when the table layout and the device allow it */
+    ESP_MODE_AUTO = 0,        /* persistent when the device can hold the grid co-resident */
     ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
     ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; workgroups meet at a
-                                 per-cluster epoch after each price update (dense layouts only;
-                                 ESP_ERR_DEVICE when the grid cannot be co-resident) */
+                                 per-cluster epoch after each price update (ESP_ERR_DEVICE when the
+                                 grid cannot be co-resident) */
 };
 
 /* Opaque context: packed table + launch plan, created by esp_create. */

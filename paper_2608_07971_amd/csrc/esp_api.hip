@@ -581,9 +581,9 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.epoch, c->base.status, B, s))) != ESP_OK)
         return st;
     // Persistent launches (one cooperative launch per chunk of up to
-    // kEtaChunk iterations) for dense tables; one launch per iteration
-    // otherwise, or when the device cannot hold the grid co-resident.
-    bool persistent = !c->pl.csr && c->mode != ESP_MODE_STREAM;
+    // kEtaChunk iterations); one launch per iteration in stream mode, or when
+    // the device cannot hold the grid co-resident.
+    bool persistent = c->mode != ESP_MODE_STREAM;
     for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
         const int n = std::min<int32_t>(kEtaChunk, iters - i0);
         if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
@@ -604,7 +604,8 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         if (persistent) {
             a.n_iters = n;
             a.epoch_base = static_cast<uint32_t>(i0);
-            const hipError_t e = launch_dense_persistent(R, c->pl.lpj, a, B, s);
+            const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
+                                           : launch_dense_persistent(R, c->pl.lpj, a, B, s);
             if (e == hipSuccess) continue;
             if (c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_DEVICE;
             (void)hipGetLastError();

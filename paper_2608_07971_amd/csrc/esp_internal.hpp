@@ -97,6 +97,7 @@ hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 // Cooperative launch (all workgroups co-resident) of a multi-iteration dense launch.
 hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,

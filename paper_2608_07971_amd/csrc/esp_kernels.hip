@@ -537,12 +537,17 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     __shared__ u128 s_acc[kBlockThreads];
     __shared__ u128 s_wsum[kBlockWaves][R];
     __shared__ u128 s_bsum[R];
+    __shared__ double s_lam[R];
+    __shared__ double s_newlam[R];
+    __shared__ int s_go;
+    __shared__ int s_stop;
 
     const int cl = blockIdx.x / a.nblk;
     const int blk = blockIdx.x - cl * a.nblk;
     if (a.flags && (a.flags[cl] & a.skip_mask)) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (threadIdx.x == 0) s_stop = 0;
 
     double lam[R];
 #pragma unroll
@@ -557,7 +562,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     const size_t lane_off = static_cast<size_t>(lane) * 4;
     const int hshift = (lane & 7) * 4;                   // this lane's 4 head bits in its word
     const double sw = a.has_pen ? a.switch_cost[cl] : 0.0;
-    auto load_tile = [&](int tl, f4 &u, f4 (&d)[R], f4 &pn, uint32_t &hw) {
+    const int stride = a.nblk * kBlockWaves;
+    const int last = a.tiles - 1;
+    auto load_tile = [&](int t, int rev, f4 &u, f4 (&d)[R], f4 &pn, uint32_t &hw) {
+        const int tl = rev ? last - t : t;
         const float *p = col + static_cast<size_t>(tl) * kTileEntries + lane_off;
         u = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
 #pragma unroll
@@ -566,23 +574,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         if (a.has_pen) pn = __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p + (R + 1) * a.col_len));
         hw = a.meta[tl].head[lane >> 3];
     };
-    const int stride = a.nblk * kBlockWaves;
-    const int last = a.tiles - 1;
-    int tile = blk * kBlockWaves + wave;
-    f4 nu, npn = {};
-    f4 nd[R];
-    uint32_t nhw = 0;
-    if (tile < a.tiles) load_tile(a.reverse ? last - tile : tile, nu, nd, npn, nhw);
-    for (; tile < a.tiles; tile += stride) {
-        const f4 u = nu, pn = npn;
-        f4 d[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) d[r] = nd[r];
-        const uint32_t hbits = (nhw >> hshift) & 0xFu;
-        if (tile + stride < a.tiles)
-            load_tile(a.reverse ? last - (tile + stride) : tile + stride, nu, nd, npn, nhw);
-        const int tl = a.reverse ? last - tile : tile;
-
+    // Score one tile, find every family's winner and stage the winners'
+    // demands (or write the choices).
+    auto process = [&](const KArgs &ai, int t, const f4 &u, const f4 (&d)[R], const f4 &pn, uint32_t hw) {
+        const int tl = ai.reverse ? last - t : t;
+        const uint32_t hbits = (hw >> hshift) & 0xFu;
         double sc[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -652,20 +648,20 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             if (q < (lane >> 3)) rank += __popc(wm[q]);
         }
         if (wbits) {
-            uint32_t hw[8];
-            if (a.choice) {
+            uint32_t hwm[8];
+            if (ai.choice) {
 #pragma unroll
-                for (int q = 0; q < 8; ++q) hw[q] = a.meta[tl].head[q];
+                for (int q = 0; q < 8; ++q) hwm[q] = a.meta[tl].head[q];
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 if (!((wbits >> i) & 1u)) continue;
-                if (a.reduce) {
+                if (ai.reduce) {
 #pragma unroll
                     for (int r = 0; r < R; ++r) s_stage[wave][rank][r] = d[r][i];
                 }
                 ++rank;
-                if (a.choice) {
+                if (ai.choice) {
                     // job = first_job + (heads at or before the slot) - 1;
                     // config = slot - (the last head at or before it)
                     const int slot = lane * 4 + i;
@@ -673,7 +669,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
                     int cnt = 0, hs = -1;
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
-                        uint32_t m = hw[q];
+                        uint32_t m = hwm[q];
                         if (q == w) m &= 0xffffffffu >> (31 - (slot & 31));
                         if (q <= w) {
                             cnt += __popc(m);
@@ -681,11 +677,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
                         }
                     }
                     const int j = static_cast<int>(a.meta[tl].first_job) + cnt - 1;
-                    a.choice[static_cast<size_t>(cl) * a.N + j] = slot - hs;
+                    ai.choice[static_cast<size_t>(cl) * a.N + j] = slot - hs;
                 }
             }
         }
-        if (a.reduce) {
+        if (ai.reduce) {
             wave_sync();
             if (acc_lane) {
 #pragma unroll 1
@@ -693,29 +689,54 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             }
             wave_sync();
         }
-    }
-    if (!a.reduce) return;
+    };
+    // One tile of prefetch: the next tile's loads are in flight while the
+    // current one is scored (the loop body is large; unrolling it costs more
+    // than the deeper prefetch gains).
+    f4 nu, npn = {};
+    f4 nd[R];
+    uint32_t nhw = 0;
+    const int tile0 = blk * kBlockWaves + wave;
+    if (tile0 < a.tiles) load_tile(tile0, a.reverse, nu, nd, npn, nhw);
+    for (int it = 0; it < a.n_iters; ++it) {
+        const KArgs ai = iteration_args<R>(a, it);
+        const int rev = ai.reverse;
+        for (int tile = tile0; tile < a.tiles; tile += stride) {
+            const f4 u = nu, pn = npn;
+            f4 d[R];
+#pragma unroll
+            for (int r = 0; r < R; ++r) d[r] = nd[r];
+            const uint32_t hw = nhw;
+            if (tile + stride < a.tiles) load_tile(tile + stride, rev, nu, nd, npn, nhw);
+            process(ai, tile, u, d, pn, hw);
+        }
+        if (!ai.reduce) return;
 
-    s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
-    __syncthreads();
-    if (threadIdx.x < kBlockWaves * R) {
-        const int w = threadIdx.x / R, r = threadIdx.x % R;
-        u128 v = 0;
+        s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
+        acc = 0;
+        __syncthreads();
+        if (threadIdx.x < kBlockWaves * R) {
+            const int w = threadIdx.x / R, r = threadIdx.x % R;
+            u128 v = 0;
 #pragma unroll 1
-        for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
-        s_wsum[w][r] = v;
-    }
-    __syncthreads();
-    if (threadIdx.x < R) {
-        u128 v = 0;
+            for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
+            s_wsum[w][r] = v;
+        }
+        __syncthreads();
+        if (threadIdx.x < R) {
+            u128 v = 0;
 #pragma unroll 1
-        for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
-        s_bsum[threadIdx.x] = v;
+            for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
+            s_bsum[threadIdx.x] = v;
+        }
+        __syncthreads();
+        const bool was_last = finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+        if (it + 1 == a.n_iters) break;
+        if (tile0 < a.tiles) load_tile(tile0, rev ^ a.sweep_alt, nu, nd, npn, nhw);
+        if (!persist_barrier<R>(a, cl, it, was_last, s_lam, &s_go, s_newlam, &s_stop)) break;
+#pragma unroll
+        for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     }
-    __syncthreads();
-    __shared__ double s_newlam[R];
-    __shared__ int s_stop;
-    finish_cluster<R>(a, cl, blk, s_bsum, s_newlam, &s_stop);
 }
 
 // ---------------------------------------------------------------------------
@@ -939,6 +960,21 @@ static hipError_t launch_csr_r(const KArgs &a, int B, hipStream_t s) {
     else
         hipLaunchKernelGGL((k_csr<R, uint64_t>), grid, block, 0, s, a);
     return hipGetLastError();
+}
+
+template <int R>
+static hipError_t launch_csr_coop_r(const KArgs &a, int B, hipStream_t s) {
+    const void *f = a.acc128 ? reinterpret_cast<const void *>(&k_csr<R, u128>)
+                             : reinterpret_cast<const void *>(&k_csr<R, uint64_t>);
+    KArgs copy = a;
+    void *args[] = {&copy};
+    return hipLaunchCooperativeKernel(f, dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), args, 0, s);
+}
+
+hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_csr_coop_r<RR>(a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
 }
 
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s) {
