@@ -1,13 +1,15 @@
 """Benchmark of the ESP hot path on one MI355X.
 
 A step is one esp_solve of the named workload: T price iterations (score ->
-select -> exact demand -> Eq. 8 update, one fused kernel launch each) plus the
-re-selection at the final prices, with the table resident in HBM.
+select -> exact demand -> Eq. 8 update, one fused pass of the kernel each) plus
+the re-selection at the final prices, with the table resident in HBM.  The
+library picks the loop driver: one launch per pass for the large tables, one
+persistent launch for all passes of the small ones.
 
 Prints one JSON line:
   value        job-configurations scored per second (whole job)
-  roofline     the fused kernel's algorithmic bytes per launch (the table:
-               (1 + R) * 4 bytes per job-configuration) over its average launch
+  roofline     the fused kernel's algorithmic bytes per pass (the table:
+               (1 + R) * 4 bytes per job-configuration) over its average pass
                duration, against the 8 TB/s HBM peak
   cpu_baseline the CPU oracle (single-threaded C) on a bounded sample of the
                same workload, in the same unit
@@ -133,20 +135,21 @@ def main() -> int:
     ms_per_step = ms_total / args.steps
     sec = ms_total / 1e3
     configs = inst.B * inst.nnz
-    launches = (T + 1) * args.steps                  # T fused iterations + the final re-selection
+    passes = (T + 1) * args.steps                    # T fused iterations + the final re-selection
+    persistent = solver.loop_driver() == esp.ESP_MODE_PERSISTENT
     # algorithmic bytes: the fp32 table read once per iteration, plus the
     # family boundaries (one 4-byte offset per job) for ragged families
     csr = inst.dense_k is None or inst.dense_k not in (4, 8, 16, 32, 64)
     pen_col = 1 if (inst.current is not None or inst.penalty is not None) else 0
-    bytes_per_launch = configs * (1 + inst.R + pen_col) * 4 + (4 * (inst.N + 1) if csr else 0)
-    avg_launch_s = sec / launches
-    achieved = bytes_per_launch / avg_launch_s / 1e9
+    bytes_per_pass = configs * (1 + inst.R + pen_col) * 4 + (4 * (inst.N + 1) if csr else 0)
+    avg_pass_s = sec / passes
+    achieved = bytes_per_pass / avg_pass_s / 1e9
     traffic = None
     if os.path.exists(args.traffic_json):
         try:
             tj = json.load(open(args.traffic_json))
             if tj.get("config") == args.config and tj.get("kernel_source_sha") == _kernel_sha():
-                traffic = tj.get("bytes_per_launch")
+                traffic = tj.get("bytes_per_pass")
         except Exception:
             traffic = None
     out = {
@@ -171,7 +174,10 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": ("k_csr" if csr else "k_dense") + " (fused score/select/demand/update)",
-                     "bytes_per_launch": bytes_per_launch, "avg_launch_us": avg_launch_s * 1e6},
+                     "driver": ("persistent: one cooperative launch runs the T passes" if persistent
+                                else "stream: one launch per pass"),
+                     "bytes_per_pass": bytes_per_pass, "avg_pass_us": avg_pass_s * 1e6,
+                     "passes_per_launch": T if persistent else 1},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = _cpu_baseline(inst, args.cpu_seconds)

@@ -58,12 +58,17 @@ enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
 
 /* Loop drivers of esp_solve (results are identical in every mode). */
 enum {
-    ESP_MODE_AUTO = 0,        /* persistent when the device can hold the grid co-resident */
+    ESP_MODE_AUTO = 0,        /* persistent for short passes (packed table of at most
+                                 ESP_AUTO_PERSISTENT_BYTES), where launch latency would dominate;
+                                 one launch per iteration otherwise, where the two drivers run at
+                                 the same speed */
     ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
     ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; workgroups meet at a
                                  per-cluster epoch after each price update (ESP_ERR_DEVICE when the
                                  grid cannot be co-resident) */
 };
+
+#define ESP_AUTO_PERSISTENT_BYTES (64u << 20)
 
 /* Opaque context: packed table + launch plan, created by esp_create. */
 typedef struct esp_ctx esp_ctx;
@@ -194,6 +199,14 @@ esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_star
  * a choice index outside its family; ESP_OK otherwise.
  */
 esp_status esp_device_status(esp_ctx *ctx, void *stream);
+
+/*
+ * esp_loop_driver: the loop driver esp_solve uses for this context,
+ * ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO resolved against the
+ * table size, and against the device once a solve has run).  Host-only.
+ * Errors: ESP_ERR_STATE (NULL context), ESP_ERR_INVALID_ARG (mode NULL).
+ */
+esp_status esp_loop_driver(const esp_ctx *ctx, int32_t *mode);
 
 /*
  * esp_set_penalties (Eq. 7): replace the penalty inputs of a context that was

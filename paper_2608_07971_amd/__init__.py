@@ -79,6 +79,7 @@ _SIGS = {
                    C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_set_penalties": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
+    "esp_loop_driver": ([C.c_void_p, C.POINTER(C.c_int32)], C.c_int),
     "esp_destroy": ([C.c_void_p], C.c_int),
     "esp_status_string": ([C.c_int], C.c_char_p),
 }
@@ -216,6 +217,12 @@ def esp_device_status(ctx: int, stream=None) -> int:
     return int(lib().esp_device_status(ctx, _stream(stream)))
 
 
+def esp_loop_driver(ctx: int) -> int:
+    mode = C.c_int32(0)
+    _check(lib().esp_loop_driver(ctx, C.byref(mode)), "esp_loop_driver")
+    return int(mode.value)
+
+
 def esp_destroy(ctx: int) -> None:
     _check(lib().esp_destroy(ctx), "esp_destroy")
 
@@ -298,3 +305,6 @@ class Solver:
 
     def device_status(self, stream=None) -> int:
         return esp_device_status(self.ctx, stream)
+
+    def loop_driver(self) -> int:
+        return esp_loop_driver(self.ctx)

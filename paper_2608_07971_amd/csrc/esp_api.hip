@@ -192,6 +192,7 @@ struct esp_ctx {
     bool eta_pending = false;
     int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
     int mode = ESP_MODE_AUTO;
+    bool fell_back = false;            // AUTO: the device refused a co-resident grid
     std::vector<int64_t> off;          // family offsets (host copy)
     std::vector<int64_t> slot_of;      // first table slot of each family
     KArgs base{};
@@ -390,6 +391,11 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     c->ws = ws;
     c->sweep = options ? options->sweep_order : 0;
     c->mode = options ? options->mode : ESP_MODE_AUTO;
+    // AUTO stays AUTO (persistent, falling back to one launch per iteration
+    // when the grid cannot be co-resident) only for short passes.
+    if (c->mode == ESP_MODE_AUTO &&
+        static_cast<size_t>(B) * pl.columns() * pl.col_len * sizeof(float) > ESP_AUTO_PERSISTENT_BYTES)
+        c->mode = ESP_MODE_STREAM;
     auto fail = [&](esp_status e) {
         if (c->h_eta) (void)hipHostFree(c->h_eta);
         if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
@@ -583,7 +589,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     // Persistent launches (one cooperative launch per chunk of up to
     // kEtaChunk iterations); one launch per iteration in stream mode, or when
     // the device cannot hold the grid co-resident.
-    bool persistent = c->mode != ESP_MODE_STREAM;
+    bool persistent = c->mode != ESP_MODE_STREAM && !c->fell_back;
     for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
         const int n = std::min<int32_t>(kEtaChunk, iters - i0);
         if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
@@ -610,6 +616,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
             if (c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_DEVICE;
             (void)hipGetLastError();
             persistent = false;                // fall back to one launch per iteration
+            c->fell_back = true;
         }
         for (int i = 0; i < n; ++i) {
             KArgs ai = a;
@@ -679,6 +686,14 @@ esp_status esp_device_status(esp_ctx *c, void *stream) {
     if (hipMemcpy(&v, d, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return ESP_ERR_DEVICE;
     if (hipMemcpy(d, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return ESP_ERR_DEVICE;
     return static_cast<esp_status>(v);
+}
+
+esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (mode == nullptr) return ESP_ERR_INVALID_ARG;
+    *mode = (c->mode == ESP_MODE_STREAM || c->fell_back) ? ESP_MODE_STREAM : ESP_MODE_PERSISTENT;
+    return ESP_OK;
 }
 
 esp_status esp_destroy(esp_ctx *c) {

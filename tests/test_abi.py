@@ -140,6 +140,8 @@ def test_null_context_is_rejected():
     assert L.esp_reduce_demand(None, None, None, None) == esp.ESP_ERR_STATE
     assert L.esp_update_prices(None, None, 1, None, None) == esp.ESP_ERR_STATE
     assert L.esp_device_status(None, None) == esp.ESP_ERR_STATE
+    mode = C.c_int32(-1)
+    assert L.esp_loop_driver(None, C.byref(mode)) == esp.ESP_ERR_STATE and mode.value == -1
     assert L.esp_destroy(None) == esp.ESP_ERR_STATE
 
 

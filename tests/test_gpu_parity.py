@@ -123,6 +123,20 @@ def test_run_to_run_and_geometry_determinism():
             assert np.array_equal(a, b)
 
 
+def test_auto_driver_follows_table_size():
+    """AUTO runs the persistent driver for short passes and one launch per
+    pass for large tables; explicit modes are kept."""
+    _say("auto driver tiny/large")
+    for name, want in (("tiny", esp.ESP_MODE_PERSISTENT), ("small", esp.ESP_MODE_PERSISTENT),
+                       ("large", esp.ESP_MODE_STREAM)):
+        s = esp.Solver(workloads.make(name))
+        assert s.loop_driver() == want, name
+        s.close()
+    s = esp.Solver(workloads.make("tiny"), mode=esp.ESP_MODE_STREAM)
+    assert s.loop_driver() == esp.ESP_MODE_STREAM
+    s.close()
+
+
 @pytest.mark.parametrize("mode", sorted(MODES))
 def test_warm_start_continues_bitwise(mode):
     inst = workloads.make("small")
