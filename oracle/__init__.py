@@ -7,7 +7,8 @@ never import it; the two share no code.
 A thin ctypes layer over ``esp_oracle.c`` (plain single-threaded C, fp64,
 ``-ffp-contract=off``), which follows the paper's Sec. 3.2 (Eq. 6-8): per-job
 argmax of utility minus price-weighted demand, exact aggregate demand, and the
-projected-subgradient price update.
+projected-subgradient price update; and Sec. 3.4's effective capacity
+(Eq. 12).
 """
 from __future__ import annotations
 
@@ -83,6 +84,8 @@ def _declare(L):
     L.orc_primal_value.restype = dbl
     L.orc_solve.argtypes = [vp, vp, i32, i32, dbl, vp, vp, vp, vp, vp, vp, vp, vp]
     L.orc_solve.restype = C.c_int
+    L.orc_effective_capacity.argtypes = [vp, C.c_int, vp, vp, dbl, vp]
+    L.orc_effective_capacity.restype = C.c_int
 
 
 def _p(a: Optional[np.ndarray]):
@@ -169,6 +172,18 @@ class Oracle:
     def primal_value(self, b: int, choice) -> float:
         ch = np.ascontiguousarray(choice, dtype=np.int32)
         return float(self.L.orc_primal_value(self._pp, b, _p(ch)))
+
+    def effective_capacity(self, b: int, capacity, gamma: float, queued=None) -> np.ndarray:
+        """Eq. 12 with this instance as the pending jobs of cluster b:
+        capacity - gamma * (exact sum over pending jobs of their componentwise
+        smallest demand vector).  queued: optional [N] mask (nonzero = pending)."""
+        cap = np.ascontiguousarray(capacity, dtype=np.float64)
+        q = None if queued is None else np.ascontiguousarray(queued, dtype=np.uint8)
+        out = np.empty(self.R, dtype=np.float64)
+        rc = self.L.orc_effective_capacity(self._pp, b, _p(q), _p(cap), float(gamma), _p(out))
+        if rc != 0:
+            raise ValueError("oracle: a pending job has no allowed configuration")
+        return out
 
     # whole loop ---------------------------------------------------------
     def solve(self, lam0=None, iters: Optional[int] = None, t_start: int = 1, tol: float = 0.0,

@@ -27,6 +27,9 @@
  *     eta_t = eta0 (fixed) or eta0 / sqrt(t) (diminishing), t = 1, 2, ...;
  *   - the loop of the tatonnement (Sec. 3.2.2/3.2.3; Alg. 1 "EspTatonnement"
  *     followed by the per-job re-selection at the final prices);
+ *   - the effective capacity of Eq. 12 (Sec. 3.4): the physical capacity
+ *     minus gamma times the exact sum, over the pending jobs, of each job's
+ *     componentwise smallest demand vector over its family;
  *   - for the pins only: the Lagrangian dual value g(lambda) of Eq. 6 at the
  *     selected configurations and the primal value sum_j u_{j,c_j} (Eq. 1).
  *
@@ -302,5 +305,51 @@ int orc_solve(const orc_problem *p, double *lam, int32_t T, int32_t t_start, dou
         if (U_out) orc_demand(p, b, ch, U_out + (int64_t)b * R);
     }
     free(ch);
+    return status;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Effective capacity (Sec. 3.4, Eq. 12).                                    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Capacity held back for the pending jobs Q at their smallest footprint:
+ *     Rmin_jr  = min over the allowed configurations k of d_jkr
+ *                (componentwise: each resource takes its own minimum),
+ *     S_r      = sum_{j in Q} Rmin_jr        (exact, rounded once),
+ *     C_eff_r  = C_r - gamma * S_r           (two rounded operations).
+ * q describes the pending jobs of cluster b (its utility is not read; the
+ * feasible mask, if any, restricts the family as in Eq. 4).  queued[j] != 0
+ * marks job j as pending; NULL means every job of q is pending.
+ * Returns 0, or -1 when a pending family has no allowed entry.
+ */
+int orc_effective_capacity(const orc_problem *q, int b, const uint8_t *queued, const double *C,
+                           double gamma, double *C_eff)
+{
+    const float *d = dem_of(q, b);
+    int r, status = 0;
+    for (r = 0; r < q->R; r++) {
+        orc_acc a;
+        int64_t j;
+        double S, g;
+        acc_clear(&a);
+        for (j = 0; j < q->N; j++) {
+            int64_t e;
+            int have = 0;
+            float m = 0.0f;
+            if (queued != NULL && queued[j] == 0) continue;
+            for (e = q->offsets[j]; e < q->offsets[j + 1]; e++) {
+                float v;
+                if (!entry_allowed(q, b, e)) continue;
+                v = d[e * q->R + r];
+                if (!have || v < m) { m = v; have = 1; }
+            }
+            if (!have) { status = -1; continue; }
+            acc_add_f32(&a, m);
+        }
+        S = acc_to_double(&a);
+        g = gamma * S;
+        C_eff[r] = C[r] - g;
+    }
     return status;
 }

@@ -39,4 +39,6 @@ double orc_primal_value(const orc_problem *p, int b, const int32_t *choice);
 int orc_solve(const orc_problem *p, double *lam, int32_t T, int32_t t_start, double tol,
               double *tr_lam, double *tr_U, int32_t *tr_choice, double *tr_dual,
               double *tr_primal, int32_t *choice_out, double *U_out, int32_t *iters_done);
+int orc_effective_capacity(const orc_problem *q, int b, const uint8_t *queued, const double *C,
+                           double gamma, double *C_eff);
 #endif

@@ -25,7 +25,9 @@ def read_golden(name: str) -> dict:
             if not ln:
                 continue
             key, _, rest = ln.partition(" ")
-            if key == "trace":
+            if key == "case":
+                out.setdefault("cases", []).append([[float(x) for x in g.split()] for g in rest.split("|")])
+            elif key == "trace":
                 out["trace"].append([[float(x) for x in g.split()] for g in rest.split("|")])
             elif "|" in rest:
                 out[key] = [[float(x) for x in g.split()] for g in rest.split("|")]
@@ -128,3 +130,37 @@ def exact_score(inst, b, e, lam, j=None) -> Fraction:
     for r in range(inst.R):
         s -= Fraction(float(lam[r])) * Fraction(float(inst.demand[b, e, r]))
     return s
+
+
+def queue_instance(offsets, demand, feasible=None, capacity=None) -> workloads.Instance:
+    """An instance holding pending jobs' families (demand only: the utility of
+    a pending job does not enter Eq. 12)."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    nnz = int(offsets[-1])
+    dem = np.asarray(demand, dtype=np.float32).reshape(1, nnz, -1)
+    R = dem.shape[2]
+    cap = (np.zeros((1, R)) if capacity is None else np.asarray(capacity, dtype=np.float64).reshape(1, R))
+    inst = workloads.Instance("queue", 0, offsets, np.zeros((1, nnz), np.float32), dem, cap,
+                              np.array([0.1]), workloads.STEP_CONST, np.zeros((1, R)), 1)
+    if feasible is not None:
+        inst.feasible = np.asarray(feasible, dtype=np.uint8).reshape(1, nnz)
+    return inst
+
+
+def brute_effective_capacity(inst, b, capacity, gamma, queued=None) -> np.ndarray:
+    """Eq. 12 in exact rationals: per pending job the componentwise minimum over
+    its allowed configurations, summed exactly, rounded once (Python's
+    correctly rounded Fraction -> float), then gamma * S and C - that in
+    binary64."""
+    off = inst.offsets
+    out = np.empty(inst.R)
+    for r in range(inst.R):
+        S = Fraction(0)
+        for j in range(inst.N):
+            if queued is not None and not queued[j]:
+                continue
+            vals = [Fraction(float(inst.demand[b, e, r])) for e in range(off[j], off[j + 1])
+                    if inst.feasible is None or inst.feasible[b, e]]
+            S += min(vals)
+        out[r] = float(capacity[r]) - float(gamma) * float(S)
+    return out

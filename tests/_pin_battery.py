@@ -12,7 +12,8 @@ import numpy as np
 
 import oracle
 import workloads
-from tests._helpers import exact_score, golden_instance, lp_optimum, read_golden
+from tests._helpers import (brute_effective_capacity, exact_score, golden_instance, lp_optimum, queue_instance,
+                           read_golden)
 
 
 def battery(L) -> None:
@@ -58,6 +59,20 @@ def battery(L) -> None:
             for r in range(inst.R):
                 vals = [float(inst.demand[0, off[j] + res["tr_choice"][t, 0, j], r]) for j in range(inst.N)]
                 assert U[r] == math.fsum(vals)
+    # effective capacity (Eq. 12): hand example and exact rationals
+    g = read_golden("hand_ceff.txt")
+    q = queue_instance(g["offsets"], g["demand"], g["feasible"], g["capacity"])
+    for gamma, queued, want in g["cases"]:
+        got = oracle.Oracle(q, L).effective_capacity(0, g["capacity"], gamma[0], np.array(queued, np.uint8))
+        assert np.array_equal(got, np.array(want))
+    rng = np.random.default_rng(9)
+    sizes = rng.integers(1, 6, 30)
+    off = np.concatenate([[0], np.cumsum(sizes)])
+    dem = (rng.random((int(off[-1]), 3)) * np.exp2(rng.integers(-20, 20, (int(off[-1]), 3)))).astype(np.float32)
+    q = queue_instance(off, dem, None, [1e3, -5.0, 0.0])
+    pend = (rng.random(30) < 0.6).astype(np.uint8)
+    got = oracle.Oracle(q, L).effective_capacity(0, q.capacity[0], 0.3, pend)
+    assert np.array_equal(got, brute_effective_capacity(q, 0, q.capacity[0], 0.3, pend))
 
 
 def main(path: str) -> int:

@@ -38,6 +38,14 @@ MUTANTS = {
     "truncating_sum": ("if (guard && (sticky || (m & 1u))) m += 1;", ";"),
     "dual_drops_capacity": ("v = v + lam[r] * p->capacity[(int64_t)b * p->R + r];", ";"),
     "select_skips_last": ("for (e = lo; e < hi; e++) {", "for (e = lo; e + 1 < hi; e++) {"),
+    "ceff_max_not_min": ("if (!have || v < m) { m = v; have = 1; }", "if (!have || v > m) { m = v; have = 1; }"),
+    "ceff_gamma_dropped": ("g = gamma * S;", "g = S;"),
+    "ceff_sign": ("C_eff[r] = C[r] - g;", "C_eff[r] = C[r] + g;"),
+    "ceff_queue_ignored": ("if (queued != NULL && queued[j] == 0) continue;", ";"),
+    "ceff_mask_ignored": ("if (!entry_allowed(q, b, e)) continue;", ";"),
+    "ceff_first_config": ("v = d[e * q->R + r];", "v = d[q->offsets[j] * q->R + r];"),
+    "ceff_whole_config": ("if (!have || v < m) { m = v; have = 1; }",
+                          "if (!have || d[e * q->R] < d[(q->offsets[j]) * q->R]) { m = v; have = 1; }"),
 }
 
 
