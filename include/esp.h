@@ -201,6 +201,47 @@ esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_star
 esp_status esp_device_status(esp_ctx *ctx, void *stream);
 
 /*
+ * esp_set_capacity (Sec. 3.2.1, C of Eq. 3): replace the physical capacity
+ * C (host [B][R], finite) of a context; the capacity used by later price
+ * updates becomes C (any effective capacity installed before is dropped).
+ * Stream-ordered after earlier work on `stream`; `capacity` may be freed when
+ * the call returns.
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG (NULL capacity),
+ * ESP_ERR_NONFINITE, ESP_ERR_RANGE (|C| > 2^200), ESP_ERR_DEVICE.
+ */
+esp_status esp_set_capacity(esp_ctx *ctx, const double *capacity, void *stream);
+
+/*
+ * esp_effective_capacity (Sec. 3.4, Eq. 12; first step of Alg. 1): reserve
+ * capacity for pending jobs at their smallest footprint,
+ *     C_eff_r = C_r - gamma * S_r,
+ *     S_r = sum over pending jobs j of min over j's allowed configurations
+ *           of d_jkr   (componentwise: each resource takes its own minimum),
+ * S_r exact and rounded once to binary64, then one rounded product and one
+ * rounded difference.  C is ctx's physical capacity (from esp_create or
+ * esp_set_capacity).  C_eff becomes the capacity of ctx's later price
+ * updates (esp_solve, esp_update_prices); a later call recomputes it from C,
+ * so epochs do not accumulate reservations.
+ *   queue         context packed (esp_create) from the pending jobs' profile
+ *                 families, same num_clusters and num_resources as ctx; only
+ *                 its demand table and feasibility mask are read (its
+ *                 utility, capacity and step rule do not enter Eq. 12).  It
+ *                 must not run other work concurrently (its cross-workgroup
+ *                 sum buffers are used).  NULL = no pending job: C_eff = C.
+ *   queued        device [B][N_queue] uint8, nonzero = pending, or NULL (every
+ *                 job of `queue` is pending).
+ *   gamma         reservation aggressiveness in [0, 1].
+ *   capacity_eff  device [B][R] receives C_eff as well, or NULL.
+ * Stream-ordered and asynchronous.  C_eff may be negative (a queue that
+ * cannot fit); the price update then raises that resource's price.
+ * Errors: ESP_ERR_STATE (NULL ctx or invalid queue), ESP_ERR_INVALID_ARG
+ * (gamma outside [0, 1] or NaN), ESP_ERR_SHAPE (B or R differ),
+ * ESP_ERR_DEVICE.
+ */
+esp_status esp_effective_capacity(esp_ctx *ctx, esp_ctx *queue, const uint8_t *queued, double gamma,
+                                  double *capacity_eff, void *stream);
+
+/*
  * esp_loop_driver: the loop driver esp_solve uses for this context,
  * ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO resolved against the
  * table size, and against the device once a solve has run).  Host-only.

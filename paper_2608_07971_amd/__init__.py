@@ -80,6 +80,9 @@ _SIGS = {
     "esp_set_penalties": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
     "esp_loop_driver": ([C.c_void_p, C.POINTER(C.c_int32)], C.c_int),
+    "esp_set_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_effective_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_double, C.c_void_p, C.c_void_p],
+                               C.c_int),
     "esp_destroy": ([C.c_void_p], C.c_int),
     "esp_status_string": ([C.c_int], C.c_char_p),
 }
@@ -223,6 +226,17 @@ def esp_loop_driver(ctx: int) -> int:
     return int(mode.value)
 
 
+def esp_set_capacity(ctx: int, capacity, stream=None) -> None:
+    cap = np.ascontiguousarray(capacity, dtype=np.float64)
+    _check(lib().esp_set_capacity(ctx, _np_ptr(cap), _stream(stream)), "esp_set_capacity")
+
+
+def esp_effective_capacity(ctx: int, queue: Optional[int], queued, gamma: float, capacity_eff=None,
+                           stream=None) -> None:
+    _check(lib().esp_effective_capacity(ctx, queue, _ptr(queued), float(gamma), _ptr(capacity_eff),
+                                        _stream(stream)), "esp_effective_capacity")
+
+
 def esp_destroy(ctx: int) -> None:
     _check(lib().esp_destroy(ctx), "esp_destroy")
 
@@ -308,3 +322,18 @@ class Solver:
 
     def loop_driver(self) -> int:
         return esp_loop_driver(self.ctx)
+
+    def set_capacity(self, capacity, stream=None) -> None:
+        esp_set_capacity(self.ctx, capacity, stream)
+
+    def effective_capacity(self, queue: Optional["Solver"], gamma: float, queued=None, stream=None):
+        """Eq. 12 with `queue` holding the pending jobs (None: no pending
+        job); installs C_eff as this context's capacity and returns it as a
+        [B, R] float64 tensor.  queued: optional uint8 [B, N_queue] tensor on
+        the device (nonzero = pending)."""
+        out = torch.empty((self.B, self.R), dtype=torch.float64, device=self.device)
+        if queued is not None:
+            assert queued.dtype == torch.uint8 and queued.is_contiguous() and queued.device == out.device
+            assert queue is not None and tuple(queued.shape) == (queue.B, queue.N)
+        esp_effective_capacity(self.ctx, None if queue is None else queue.ctx, queued, gamma, out, stream)
+        return out

@@ -38,7 +38,7 @@ struct Plan {
     int nblk = 0;       // workgroups per cluster
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, total = 0;
+           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -150,6 +150,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_epoch = o; o = align_up(o + B * sizeof(uint32_t));
     pl->o_swc = o;   o = align_up(o + B * sizeof(double));
     pl->o_status = o; o = align_up(o + sizeof(int32_t));
+    pl->o_capp = o;  o = align_up(o + B * R * sizeof(double));
     pl->total = o;
     return ESP_OK;
 }
@@ -486,6 +487,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                                  hipMemcpyHostToDevice, s) == hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_cap, cap.data(), sizeof(double) * cap.size(), hipMemcpyHostToDevice, s) ==
                       hipSuccess &&
+                  hipMemcpyAsync(ws + pl.o_capp, cap.data(), sizeof(double) * cap.size(), hipMemcpyHostToDevice,
+                                 s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_tick, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
@@ -686,6 +689,59 @@ esp_status esp_device_status(esp_ctx *c, void *stream) {
     if (hipMemcpy(&v, d, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return ESP_ERR_DEVICE;
     if (hipMemcpy(d, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return ESP_ERR_DEVICE;
     return static_cast<esp_status>(v);
+}
+
+esp_status esp_set_capacity(esp_ctx *c, const double *capacity, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (capacity == nullptr) return ESP_ERR_INVALID_ARG;
+    const size_t n = static_cast<size_t>(c->pl.B) * c->pl.R;
+    for (size_t i = 0; i < n; ++i) {
+        if (!std::isfinite(capacity[i])) return ESP_ERR_NONFINITE;
+        if (std::fabs(capacity[i]) > 0x1p200) return ESP_ERR_RANGE;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // Stage through the pinned step-size buffer (B * kEtaChunk >= B * R doubles).
+    if (c->eta_pending) {
+        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
+        c->eta_pending = false;
+    }
+    std::memcpy(c->h_eta, capacity, sizeof(double) * n);
+    if (hipMemcpyAsync(c->ws + c->pl.o_capp, c->h_eta, sizeof(double) * n, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipMemcpyAsync(c->ws + c->pl.o_cap, c->ws + c->pl.o_capp, sizeof(double) * n, hipMemcpyDeviceToDevice, s) !=
+            hipSuccess ||
+        hipEventRecord(c->eta_ev, s) != hipSuccess)
+        return ESP_ERR_DEVICE;
+    c->eta_pending = true;
+    return ESP_OK;
+}
+
+esp_status esp_effective_capacity(esp_ctx *c, esp_ctx *queue, const uint8_t *queued, double gamma,
+                                  double *capacity_eff, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (queue != nullptr && (st = check_ctx(queue)) != ESP_OK) return st;
+    if (!(gamma >= 0.0 && gamma <= 1.0)) return ESP_ERR_INVALID_ARG;     // also rejects NaN
+    if (queue != nullptr && (queue->pl.B != c->pl.B || queue->pl.R != c->pl.R)) return ESP_ERR_SHAPE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int B = c->pl.B, R = c->pl.R;
+    double *cap = reinterpret_cast<double *>(c->ws + c->pl.o_cap);
+    const double *capp = reinterpret_cast<const double *>(c->ws + c->pl.o_capp);
+    if (queue == nullptr) {
+        // No pending jobs: C_eff = C.
+        const size_t bytes = sizeof(double) * B * R;
+        if (hipMemcpyAsync(cap, capp, bytes, hipMemcpyDeviceToDevice, s) != hipSuccess) return ESP_ERR_DEVICE;
+        if (capacity_eff && hipMemcpyAsync(capacity_eff, capp, bytes, hipMemcpyDeviceToDevice, s) != hipSuccess)
+            return ESP_ERR_DEVICE;
+        return ESP_OK;
+    }
+    ReserveArgs ra;
+    ra.queued = queued;
+    ra.cap_phys = capp;
+    ra.cap_eff = cap;
+    ra.out = capacity_eff;
+    ra.gamma = gamma;
+    return dev(launch_reserve(R, queue->base, ra, B, s));
 }
 
 esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {

@@ -92,6 +92,17 @@ struct KArgs {
 
 constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
 
+// Extra arguments of the effective-capacity kernel (Eq. 12): the KArgs of the
+// pending jobs' context supply the table, the fixed-point windows and the
+// cross-workgroup sum buffers.
+struct ReserveArgs {
+    const uint8_t *queued;         // [B][N] nonzero = pending, or NULL (all pending)
+    const double *cap_phys;        // [B][R] physical capacity C
+    double *cap_eff;               // [B][R] receives C - gamma * S (the active context's capacity)
+    double *out;                   // [B][R] copy for the caller, or NULL
+    double gamma;                  // reservation aggressiveness in [0, 1]
+};
+
 // Host-side launchers (esp_kernels.hip).
 hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 // Cooperative launch (all workgroups co-resident) of a multi-iteration dense launch.
@@ -99,6 +110,7 @@ hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStr
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,
                           uint32_t *epoch, int32_t *status, int B, hipStream_t s);

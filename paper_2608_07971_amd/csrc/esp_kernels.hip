@@ -177,7 +177,11 @@ __device__ __forceinline__ int complete_cluster(const KArgs &a, int cl, const in
     return stop;
 }
 
-// bsum[r] (LDS) holds this workgroup's 128-bit sum for resource r.
+// Cross-workgroup exact sums of one cluster.  bsum[r] (LDS) holds this
+// workgroup's 128-bit sum for resource r.  In the workgroup that finishes
+// last, thread r < R runs done(r, total_r) with the cluster's total; the
+// function returns true there (after a workgroup barrier) and false in every
+// other workgroup.
 //
 // Ordering across the 8 XCDs (each with its own L2) without cache-wide
 // writeback or invalidation: wavefront 0 publishes the partial with
@@ -186,22 +190,17 @@ __device__ __forceinline__ int complete_cluster(const KArgs &a, int cl, const in
 // (s_waitcnt vmcnt(0) on the returned values) before it takes a ticket with
 // an agent-scope atomic add.  The workgroup that draws the last ticket reads
 // every partial with agent-scope atomic loads, which bypass the non-coherent
-// caches.
-// s_newlam / s_stop (LDS) receive the new prices and the stop decision in
-// the last workgroup.
-template <int R>
-__device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum, double *s_newlam, int *s_stop) {
+// caches, and resets the ticket for the next use.
+template <int R, typename Done>
+__device__ __forceinline__ bool cluster_sums(const KArgs &a, int cl, int blk, const u128 *bsum, Done &&done) {
     __shared__ int s_last;
     __shared__ u128 s_red[kBlockThreads];
-    __shared__ int s_ok[R];
     const int t = threadIdx.x;
     if (a.nblk == 1) {
         // One workgroup per cluster: its own sums are the totals.
         if (t < R) s_red[t] = bsum[t];
         __syncthreads();
-        if (t < R) complete_resource<R>(a, cl, t, s_red[t], s_ok, s_newlam);
-        __syncthreads();
-        if (t == 0) *s_stop = complete_cluster<R>(a, cl, s_ok);
+        if (t < R) done(t, s_red[t]);
         __syncthreads();
         return true;
     }
@@ -255,15 +254,29 @@ __device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
         u128 tot = 0;
 #pragma unroll 1
         for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
-        complete_resource<R>(a, cl, t, tot, s_ok, s_newlam);
+        done(t, tot);
     }
-    __syncthreads();
     if (t == 0) {
-        // ready for the next iteration
+        // ready for the next use
         const unsigned o = __hip_atomic_exchange(&a.tickets[cl], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         asm volatile("s_waitcnt vmcnt(0)" : : "v"(o) : "memory");
-        *s_stop = complete_cluster<R>(a, cl, s_ok);
     }
+    __syncthreads();
+    return true;
+}
+
+// The demand sums of one iteration: U, the Eq. 8 update and the per-cluster
+// bookkeeping in the last workgroup.  s_newlam / s_stop (LDS) receive the new
+// prices and the stop decision there.
+template <int R>
+__device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum, double *s_newlam, int *s_stop) {
+    __shared__ int s_ok[R];
+    const bool last = cluster_sums<R>(a, cl, blk, bsum, [&](int r, u128 tot) {
+        complete_resource<R>(a, cl, r, tot, s_ok, s_newlam);
+    });
+    if (!last) return false;
+    if (threadIdx.x == 0) *s_stop = complete_cluster<R>(a, cl, s_ok);
+    __syncthreads();
     return true;
 }
 
@@ -798,6 +811,136 @@ __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Effective capacity (Sec. 3.4, Eq. 12)
+// ---------------------------------------------------------------------------
+
+// C_eff_r = C_r - gamma * S_r, S_r = sum over pending jobs j of
+// min over j's allowed configurations of d_jkr (the componentwise smallest
+// footprint), over the pending jobs' own packed table.  A wavefront takes one
+// tile at a time: each lane folds its 4 entries into one minimum per job
+// piece (entries of one job are adjacent) and merges it into the tile's
+// per-job minima in LDS with an unsigned atomic minimum (demands are
+// non-negative floats with +0.0 for zero, whose bit patterns order like the
+// values); the lanes then add the minima of pending jobs to exact fixed-point
+// accumulators.  Masked configurations and padding carry a utility of -inf
+// (dense padding: job index >= N) and are skipped.
+template <int R, typename A>
+__global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs ra) {
+    constexpr uint32_t kInf = 0x7f800000u;
+    __shared__ uint32_t s_min[kBlockWaves][kTileEntries][R];
+    __shared__ u128 s_part[kBlockWaves][R];
+    __shared__ u128 s_bsum[R];
+    const int cl = blockIdx.x / a.nblk;
+    const int blk = blockIdx.x - cl * a.nblk;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const float *col = a.table + cl * a.cluster_stride;
+    const uint8_t *pend = ra.queued ? ra.queued + static_cast<size_t>(cl) * a.N : nullptr;
+    int sh[R];
+    A acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        sh[r] = a.shift[cl * R + r];
+        acc[r] = 0;
+    }
+    uint32_t *mins = &s_min[wave][0][0];
+    for (int i = lane; i < kTileEntries * R; i += kWaveSize) mins[i] = kInf;
+    wave_sync();
+    const int jpt = a.K > 0 ? kTileEntries / a.K : 0;          // dense: jobs per tile
+    for (int tile = blk * kBlockWaves + wave; tile < a.tiles; tile += a.nblk * kBlockWaves) {
+        const size_t base = static_cast<size_t>(tile) * kTileEntries + static_cast<size_t>(lane) * 4;
+        const f4 u = *reinterpret_cast<const f4 *>(col + base);
+        f4 d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = *reinterpret_cast<const f4 *>(col + (r + 1) * a.col_len + base);
+        int first_job, njobs, jt;
+        uint32_t heads;                        // bit i: entry 4*lane + i starts a job
+        if (a.K > 0) {
+            first_job = tile * jpt;
+            njobs = min(jpt, a.N - first_job);
+            jt = (lane * 4) / a.K;
+            heads = 0;                         // K >= 4: a lane's 4 entries share one job
+        } else {
+            const TileMeta &m = a.meta[tile];
+            const int e0 = lane * 4, w = e0 >> 5, bit = e0 & 31;
+            int before = 0, total = 0;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int c = __popc(m.head[q]);
+                total += c;
+                before += (q < w) ? c : 0;
+            }
+            const uint32_t word = m.head[w];
+            const uint32_t upto = (bit == 31) ? 0xffffffffu : ((2u << bit) - 1u);
+            first_job = static_cast<int>(m.first_job);
+            njobs = total;
+            jt = before + __popc(word & upto) - 1; // entry 0 of a tile always starts a job
+            heads = (word >> bit) & 0xfu;
+        }
+        uint32_t mn[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) mn[r] = kInf;
+        auto flush = [&]() {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (mn[r] != kInf) atomicMin(&s_min[wave][jt][r], mn[r]);
+        };
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (i > 0 && ((heads >> i) & 1u)) {
+                flush();
+                ++jt;
+#pragma unroll
+                for (int r = 0; r < R; ++r) mn[r] = kInf;
+            }
+            const bool valid = (u[i] != -__builtin_inff()) && (jt < njobs);
+            if (valid) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) mn[r] = min(mn[r], __float_as_uint(d[r][i]));
+            }
+        }
+        flush();
+        wave_sync();
+        for (int q = lane; q < njobs; q += kWaveSize) {
+            const bool take = !pend || pend[first_job + q] != 0;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const uint32_t m = s_min[wave][q][r];
+                s_min[wave][q][r] = kInf;
+                if (take && m != kInf) acc[r] += fx_of<A>(__uint_as_float(m), sh[r]);
+            }
+        }
+        wave_sync();
+    }
+    // workgroup sums: wavefront tree over lanes, then the 4 wavefronts in order
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        u128 v = static_cast<u128>(acc[r]);
+#pragma unroll
+        for (int off = kWaveSize / 2; off > 0; off >>= 1) {
+            const unsigned long long lo = __shfl_down(static_cast<unsigned long long>(v), off);
+            const unsigned long long hi = __shfl_down(static_cast<unsigned long long>(v >> 64), off);
+            v += (static_cast<u128>(hi) << 64) | lo;
+        }
+        if (lane == 0) s_part[wave][r] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < R) {
+        u128 t = 0;
+        for (int w = 0; w < kBlockWaves; ++w) t += s_part[w][threadIdx.x];
+        s_bsum[threadIdx.x] = t;
+    }
+    __syncthreads();
+    cluster_sums<R>(a, cl, blk, s_bsum, [&](int r, u128 tot) {
+        const double S = fx_to_double(tot, a.shift[cl * R + r]);
+        const double g = ra.gamma * S;
+        const double ce = ra.cap_phys[cl * R + r] - g;
+        ra.cap_eff[cl * R + r] = ce;
+        if (ra.out) ra.out[cl * R + r] = ce;
+    });
+}
+
+// ---------------------------------------------------------------------------
 // Granular price update (esp_update_prices) and price validation
 // ---------------------------------------------------------------------------
 
@@ -921,6 +1064,22 @@ static hipError_t launch_gather_r(const KArgs &a, int B, hipStream_t s) {
 
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s) {
 #define CALL(RR) launch_gather_r<RR>(a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_reserve_r(const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
+    if (a.acc128)
+        hipLaunchKernelGGL((k_reserve<R, u128>), grid, block, 0, s, a, ra);
+    else
+        hipLaunchKernelGGL((k_reserve<R, uint64_t>), grid, block, 0, s, a, ra);
+    return hipGetLastError();
+}
+
+hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s) {
+#define CALL(RR) launch_reserve_r<RR>(a, ra, B, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }

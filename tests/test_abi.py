@@ -142,6 +142,9 @@ def test_null_context_is_rejected():
     assert L.esp_device_status(None, None) == esp.ESP_ERR_STATE
     mode = C.c_int32(-1)
     assert L.esp_loop_driver(None, C.byref(mode)) == esp.ESP_ERR_STATE and mode.value == -1
+    cap = (C.c_double * 2)(1.0, 2.0)
+    assert L.esp_set_capacity(None, cap, None) == esp.ESP_ERR_STATE
+    assert L.esp_effective_capacity(None, None, None, 0.5, None, None) == esp.ESP_ERR_STATE
     assert L.esp_destroy(None) == esp.ESP_ERR_STATE
 
 

@@ -1,0 +1,177 @@
+"""GPU parity of the effective-capacity pre-pass (Sec. 3.4, Eq. 12) through
+the C-ABI against the oracle, and of the ESP loop that runs on it.
+
+C_eff is bitwise equal on both sides: the per-job minima are exact, their
+sum is exact and rounded once, then one product and one difference."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_07971_amd as esp
+import workloads
+from tests._helpers import queue_instance, read_golden
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def _with_mask(inst, seed, frac=0.3):
+    """Mark about `frac` of the configurations infeasible (Eq. 4), keeping at
+    least one allowed configuration per family."""
+    rng = np.random.default_rng(seed)
+    f = (rng.random((inst.B, inst.nnz)) >= frac).astype(np.uint8)
+    off = inst.offsets
+    for b in range(inst.B):
+        for j in range(inst.N):
+            if not f[b, off[j]:off[j + 1]].any():
+                f[b, off[j] + rng.integers(0, off[j + 1] - off[j])] = 1
+    inst.feasible = f
+    return inst
+
+
+def _pending(inst, seed, frac=0.6):
+    rng = np.random.default_rng(seed)
+    return (rng.random((inst.B, inst.N)) < frac).astype(np.uint8)
+
+
+def _check(a, q, cap, queue, gamma, pend=None):
+    """Run the pre-pass on the GPU (active solver a, queue solver q packed
+    from `queue`, physical capacity cap [B, R]) and compare every cluster
+    with the oracle."""
+    qo = oracle.Oracle(queue)
+    qd = None if pend is None else torch.from_numpy(pend).cuda()
+    got = a.effective_capacity(q, gamma, qd).cpu().numpy()
+    torch.cuda.synchronize()
+    for b in range(queue.B):
+        want = qo.effective_capacity(b, cap[b], gamma, None if pend is None else pend[b])
+        assert np.array_equal(got[b], want), (b, got[b], want)
+    return got
+
+
+def test_hand_example_on_gpu():
+    g = read_golden("hand_ceff.txt")
+    qi = queue_instance(g["offsets"], g["demand"], g["feasible"], g["capacity"])
+    _say("C_eff hand example")
+    active = workloads.random_small(1, 20, 4, 3)
+    active.capacity = np.array(g["capacity"], dtype=np.float64).reshape(1, 3)
+    a, q = esp.Solver(active), esp.Solver(qi)
+    for gamma, queued, want in g["cases"]:
+        pend = np.array(queued, dtype=np.uint8).reshape(1, -1)
+        got = a.effective_capacity(q, gamma[0], torch.from_numpy(pend).cuda()).cpu().numpy()
+        assert np.array_equal(got[0], np.array(want)), (gamma, queued, got)
+
+
+QUEUE_CASES = {
+    "csr_r3": lambda: _with_mask(workloads.random_small(11, 3001, 9, 3), 1),
+    "csr_r8_batched": lambda: _with_mask(workloads.random_small(12, 700, 40, 8, n_clusters=3), 2),
+    "dense_k4_r1": lambda: workloads.random_small(13, 1025, 4, 1, dense=True),
+    "dense_k8_r5_mask": lambda: _with_mask(workloads.random_small(14, 999, 8, 5, dense=True), 3),
+    "dense_k16_r2": lambda: workloads.random_small(15, 777, 16, 2, dense=True, n_clusters=2),
+    "dense_k32_r4": lambda: workloads.random_small(16, 300, 32, 4, dense=True),
+    "dense_k64_r8_mask": lambda: _with_mask(workloads.random_small(17, 401, 64, 8, dense=True), 4),
+    "ragged_5000": lambda: workloads.make("ragged", n_jobs=5000),
+    "tiny": lambda: workloads.make("tiny"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(QUEUE_CASES))
+def test_effective_capacity_matches_oracle(name):
+    queue = QUEUE_CASES[name]()
+    _say(f"C_eff {name}: B={queue.B} N={queue.N} R={queue.R} nnz={queue.nnz}")
+    active = workloads.random_small(2, 50, 5, queue.R, n_clusters=queue.B)
+    a, q = esp.Solver(active), esp.Solver(queue)
+    for gamma in (0.0, 0.25, 1.0 / 3.0, 1.0):
+        _check(a, q, active.capacity, queue, gamma)
+        _check(a, q, active.capacity, queue, gamma, _pending(queue, 7))
+    _check(a, q, active.capacity, queue, 0.5, np.zeros((queue.B, queue.N), np.uint8))
+    assert a.device_status() == 0 and q.device_status() == 0
+
+
+def test_wide_value_span_uses_128_bit_sums():
+    """Demands spread over 2^-40 .. 2^40: the packer picks 128-bit
+    accumulators; the sum is still exact."""
+    rng = np.random.default_rng(3)
+    queue = workloads.random_small(18, 2000, 12, 4)
+    queue.demand = (queue.demand * np.exp2(rng.integers(-40, 40, queue.demand.shape))).astype(np.float32)
+    _say("C_eff wide span")
+    active = workloads.random_small(2, 50, 5, 4)
+    active.capacity = np.full((1, 4), 1e15)
+    a, q = esp.Solver(active), esp.Solver(queue)
+    for gamma in (0.3, 1.0):
+        _check(a, q, active.capacity, queue, gamma, _pending(queue, 8))
+
+
+def test_solve_runs_on_effective_capacity():
+    """After the pre-pass the ESP loop uses C_eff: its trace equals the
+    oracle's on an instance whose capacity is the oracle's C_eff; NULL queue
+    and esp_set_capacity restore C."""
+    active = workloads.make("ragged", n_jobs=3000)
+    queue = workloads.make("ragged", n_jobs=800, seed=99)
+    _say("solve on C_eff: ragged 3000, queue 800")
+    a, q = esp.Solver(active), esp.Solver(queue)
+    pend = _pending(queue, 9, 0.5)
+    ceff = _check(a, q, active.capacity, queue, 0.5, pend)
+    T = 60
+    g = a.solve(a.prices(active.lam0), T, trace=True, trace_choice=True)
+    torch.cuda.synchronize()
+    shifted = workloads.make("ragged", n_jobs=3000)
+    shifted.capacity = ceff.copy()
+    ref = oracle.Oracle(shifted).solve(iters=T, trace_choice=True)
+    assert np.array_equal(g["tr_choice"].cpu().numpy(), ref["tr_choice"])
+    assert np.array_equal(g["tr_lam"].cpu().numpy(), ref["tr_lam"])
+    # no pending job: C_eff = C
+    back = a.effective_capacity(None, 0.5).cpu().numpy()
+    assert np.array_equal(back, active.capacity)
+    g2 = a.solve(a.prices(active.lam0), T, trace=True)
+    ref2 = oracle.Oracle(active).solve(iters=T)
+    torch.cuda.synchronize()
+    assert np.array_equal(g2["tr_lam"].cpu().numpy(), ref2["tr_lam"])
+    # a new physical capacity replaces C and drops C_eff
+    a.effective_capacity(q, 1.0)
+    newcap = active.capacity * 0.75
+    a.set_capacity(newcap)
+    g3 = a.solve(a.prices(active.lam0), T, trace=True)
+    torch.cuda.synchronize()
+    shifted.capacity = newcap
+    ref3 = oracle.Oracle(shifted).solve(iters=T)
+    assert np.array_equal(g3["tr_lam"].cpu().numpy(), ref3["tr_lam"])
+    _check(a, q, newcap, queue, 0.25, pend)
+
+
+def test_effective_capacity_argument_errors():
+    active = workloads.random_small(3, 40, 4, 3)
+    queue = workloads.random_small(4, 30, 4, 3)
+    other_r = workloads.random_small(5, 30, 4, 2)
+    _say("C_eff argument errors")
+    a, q = esp.Solver(active), esp.Solver(queue)
+    q2 = esp.Solver(other_r)
+    L = esp.lib()
+    for gamma in (-0.1, 1.5, float("nan"), float("inf")):
+        assert L.esp_effective_capacity(a.ctx, q.ctx, None, gamma, None, None) == esp.ESP_ERR_INVALID_ARG
+    assert L.esp_effective_capacity(a.ctx, q2.ctx, None, 0.5, None, None) == esp.ESP_ERR_SHAPE
+    bad = np.array([1.0, float("nan"), 2.0])
+    with pytest.raises(esp.EspError) as e:
+        a.set_capacity(bad)
+    assert e.value.code == esp.ESP_ERR_NONFINITE
+    torch.cuda.synchronize()
+    assert a.device_status() == 0
+
+
+def test_fullsize_queues():
+    """The Ragged (1,048,576 ragged families, R = 6) and Large (262,144 x 64,
+    R = 8) tables as pending queues, in the launch configuration the library
+    picks: C_eff bitwise equal to the oracle's."""
+    for name in ("ragged", "large"):
+        queue = workloads.make(name)
+        _say(f"C_eff full-size queue {name}")
+        active = workloads.random_small(2, 50, 5, queue.R)
+        active.capacity = np.asarray(queue.capacity, dtype=np.float64).copy()
+        a, q = esp.Solver(active), esp.Solver(queue)
+        _check(a, q, active.capacity, queue, 0.5)
+        _check(a, q, active.capacity, queue, 1.0, _pending(queue, 10, 0.3))
+        q.close()
+        a.close()
