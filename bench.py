@@ -46,6 +46,11 @@ def _parse():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (10 times): the reference kernel "
                          "whose FETCH_SIZE / WRITE_SIZE counters scale the fused kernel's")
+    ap.add_argument("--epochs", type=int, default=0, metavar="E",
+                    help="instead of the default line: E scheduling epochs of an active market plus a pending "
+                         "queue (C_eff of Eq. 12 each epoch, then esp_solve to tol 1e-3 from cold and from "
+                         "warm prices); prints iterations to converge and epoch times")
+    ap.add_argument("--epoch-jobs", type=int, default=1048576, help="active jobs of the --epochs market")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_large.json"),
                     help="HBM bytes per launch measured with rocprofv3 counters, if present")
     return ap.parse_args()
@@ -98,6 +103,9 @@ def main() -> int:
 
     import paper_2608_07971_amd as esp
     import workloads
+
+    if args.epochs:
+        return _epochs(args, esp, workloads, np, torch)
 
     t_gen = time.perf_counter()
     kw = {}
@@ -183,6 +191,77 @@ def main() -> int:
         out["cpu_baseline"] = _cpu_baseline(inst, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     solver.close()
+    return 0
+
+
+def _epochs(args, esp, workloads, np, torch) -> int:
+    """Scheduling epochs (Sec. 3.4, Alg. 1 first step and warm start): each
+    epoch recomputes C_eff from the epoch's pending set (gamma = 0.5), then
+    runs the tatonnement to tol = 1e-3 (at most 1000 iterations) from
+    lambda = 0 (cold) and from the previous epoch's prices (warm, t restarts
+    at 1).  Times with HIP events on the solve stream; the first epoch is
+    also run once untimed."""
+    E, TOL, GAMMA, TMAX = args.epochs, 1e-3, 0.5, 1000
+    act, que = workloads.epoch_market(args.epoch_jobs)
+    pend = torch.from_numpy(workloads.epoch_pending(que.N, E)).cuda().contiguous()
+    a = esp.Solver(act)
+    q = esp.Solver(que)
+    stream = torch.cuda.Stream()
+    print(f"[bench] epochs: active N={act.N} nnz={act.nnz} queue N={que.N} nnz={que.nnz} R={act.R} E={E}",
+          file=sys.stderr, flush=True)
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            e0.record(stream)
+            out = fn()
+            e1.record(stream)
+        torch.cuda.synchronize()
+        return out, e0.elapsed_time(e1)
+
+    def solve(lam0):
+        lam = lam0.clone()
+        g = a.solve(lam, TMAX, tol=TOL, stream=stream)
+        return lam, g
+
+    zero = a.prices(np.zeros((1, act.R)))
+    # untimed warm-up of every kernel involved
+    a.effective_capacity(q, GAMMA, pend[0:1].clone())
+    solve(zero)
+    torch.cuda.synchronize()
+    rows, lam_w = [], None
+    for e in range(E):
+        pe = pend[e:e + 1].clone()
+        _, ms_c = timed(lambda: a.effective_capacity(q, GAMMA, pe, stream=stream))
+        (lam_c, gc), ms_cold = timed(lambda: solve(zero))
+        (lam_w, gw), ms_warm = timed(lambda: solve(lam_c if lam_w is None else lam_w))
+        rows.append((ms_c, int(gc["iters_done"][0]), ms_cold, int(gw["iters_done"][0]), ms_warm))
+        print(f"[bench] epoch {e}: C_eff {ms_c * 1e3:.1f} us, cold {rows[-1][1]} it {ms_cold:.3f} ms, "
+              f"warm {rows[-1][3]} it {ms_warm:.3f} ms", file=sys.stderr, flush=True)
+    assert a.device_status() == 0 and q.device_status() == 0
+    later = rows[1:] if E > 1 else rows
+    mean = lambda i: sum(r[i] for r in later) / len(later)
+    ceff_bytes = que.nnz * (1 + que.R) * 4 + que.N
+    out = {
+        "metric": "price iterations to converge per scheduling epoch (tol 1e-3), warm vs cold start",
+        "value": mean(3),
+        "unit": "iterations (warm start, mean over epochs 1..E-1)",
+        "higher_is_better": False,
+        "n_gpus": 1, "steps": E, "warmup": 1, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"epoch market: {act.N} active jobs x Geo(0.08) configs x {act.R} resources "
+                               f"(unit share per job), queue {que.N} jobs, gamma {GAMMA}, tol {TOL}",
+                   "epochs": E},
+        "cold_iters": mean(1), "warm_iters": mean(3),
+        "epoch_ms_cold": mean(0) + mean(2), "epoch_ms_warm": mean(0) + mean(4),
+        "ceff_us": 1e3 * mean(0),
+        "ceff_gbs": ceff_bytes / (mean(0) * 1e-3) / 1e9,
+        "ceff_bytes": ceff_bytes,
+        "per_epoch": [{"ceff_us": 1e3 * r[0], "cold_iters": r[1], "cold_ms": r[2], "warm_iters": r[3],
+                       "warm_ms": r[4]} for r in rows],
+    }
+    print(json.dumps(out), flush=True)
+    a.close()
+    q.close()
     return 0
 
 

@@ -59,9 +59,12 @@ enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
 /* Loop drivers of esp_solve (results are identical in every mode). */
 enum {
     ESP_MODE_AUTO = 0,        /* persistent for short passes (packed table of at most
-                                 ESP_AUTO_PERSISTENT_BYTES), where launch latency would dominate;
-                                 one launch per iteration otherwise, where the two drivers run at
-                                 the same speed */
+                                 ESP_AUTO_PERSISTENT_BYTES), where launch latency would dominate,
+                                 and for solves with tol > 0 (the loop ends on the device once
+                                 every cluster has converged); one launch per iteration
+                                 otherwise, where the two drivers run at the same speed; falls
+                                 back to one launch per iteration when the device cannot hold
+                                 the grid co-resident */
     ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
     ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; workgroups meet at a
                                  per-cluster epoch after each price update (ESP_ERR_DEVICE when the
@@ -242,9 +245,10 @@ esp_status esp_effective_capacity(esp_ctx *ctx, esp_ctx *queue, const uint8_t *q
                                   double *capacity_eff, void *stream);
 
 /*
- * esp_loop_driver: the loop driver esp_solve uses for this context,
- * ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO resolved against the
- * table size, and against the device once a solve has run).  Host-only.
+ * esp_loop_driver: the loop driver esp_solve uses for this context's solves
+ * with tol = 0, ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO
+ * resolved against the table size, and against the device once a solve has
+ * run).  Host-only.
  * Errors: ESP_ERR_STATE (NULL context), ESP_ERR_INVALID_ARG (mode NULL).
  */
 esp_status esp_loop_driver(const esp_ctx *ctx, int32_t *mode);

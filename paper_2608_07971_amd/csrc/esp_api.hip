@@ -193,6 +193,7 @@ struct esp_ctx {
     bool eta_pending = false;
     int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
     int mode = ESP_MODE_AUTO;
+    bool auto_mode = false;            // the caller asked for ESP_MODE_AUTO
     bool fell_back = false;            // AUTO: the device refused a co-resident grid
     std::vector<int64_t> off;          // family offsets (host copy)
     std::vector<int64_t> slot_of;      // first table slot of each family
@@ -392,8 +393,11 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     c->ws = ws;
     c->sweep = options ? options->sweep_order : 0;
     c->mode = options ? options->mode : ESP_MODE_AUTO;
+    c->auto_mode = c->mode == ESP_MODE_AUTO;
     // AUTO stays AUTO (persistent, falling back to one launch per iteration
-    // when the grid cannot be co-resident) only for short passes.
+    // when the grid cannot be co-resident) only for short passes; solves with
+    // a stop tolerance use the persistent driver in any case (the loop then
+    // ends on the device as soon as every cluster has converged).
     if (c->mode == ESP_MODE_AUTO &&
         static_cast<size_t>(B) * pl.columns() * pl.col_len * sizeof(float) > ESP_AUTO_PERSISTENT_BYTES)
         c->mode = ESP_MODE_STREAM;
@@ -592,7 +596,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     // Persistent launches (one cooperative launch per chunk of up to
     // kEtaChunk iterations); one launch per iteration in stream mode, or when
     // the device cannot hold the grid co-resident.
-    bool persistent = c->mode != ESP_MODE_STREAM && !c->fell_back;
+    bool persistent = !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
     for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
         const int n = std::min<int32_t>(kEtaChunk, iters - i0);
         if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
@@ -616,7 +620,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
             const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
                                            : launch_dense_persistent(R, c->pl.lpj, a, B, s);
             if (e == hipSuccess) continue;
-            if (c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_DEVICE;
+            if (!c->auto_mode) return ESP_ERR_DEVICE;
             (void)hipGetLastError();
             persistent = false;                // fall back to one launch per iteration
             c->fell_back = true;

@@ -175,3 +175,41 @@ def test_fullsize_queues():
         _check(a, q, active.capacity, queue, 1.0, _pending(queue, 10, 0.3))
         q.close()
         a.close()
+
+
+def test_epochs_cold_and_warm_match_oracle():
+    """Scheduling epochs on the unit-share market: per epoch C_eff, then the
+    tatonnement to tol from zero prices and from the previous epoch's
+    prices; iteration counts, final prices and choices equal the oracle's."""
+    act, que = workloads.epoch_market(3000)
+    E = 3
+    pend = workloads.epoch_pending(que.N, E)
+    _say(f"epochs: active {act.N}, queue {que.N}")
+    a, q = esp.Solver(act), esp.Solver(que)
+    qo = oracle.Oracle(que)
+    lam_w = None
+    lam_w_ref = None
+    for e in range(E):
+        ce = a.effective_capacity(q, 0.5, torch.from_numpy(pend[e:e + 1].copy()).cuda()).cpu().numpy()
+        want = qo.effective_capacity(0, act.capacity[0], 0.5, pend[e])
+        assert np.array_equal(ce[0], want)
+        shifted = workloads.epoch_market(3000)[0]
+        shifted.capacity = ce.copy()
+        o = oracle.Oracle(shifted)
+        rc = o.solve(iters=1000, tol=1e-3, trace=False)
+        lam = a.prices(np.zeros((1, act.R)))
+        gc = a.solve(lam, 1000, tol=1e-3)
+        torch.cuda.synchronize()
+        assert int(gc["iters_done"][0]) == int(rc["iters_done"][0]) < 1000
+        assert np.array_equal(lam.cpu().numpy(), rc["lam"])
+        assert np.array_equal(gc["choice"].cpu().numpy(), rc["choice"])
+        start = rc["lam"] if lam_w_ref is None else lam_w_ref
+        rw = o.solve(lam0=start, iters=1000, tol=1e-3, trace=False)
+        lam2 = a.prices(start)
+        gw = a.solve(lam2, 1000, tol=1e-3)
+        torch.cuda.synchronize()
+        assert int(gw["iters_done"][0]) == int(rw["iters_done"][0])
+        assert np.array_equal(lam2.cpu().numpy(), rw["lam"])
+        assert np.array_equal(gw["choice"].cpu().numpy(), rw["choice"])
+        lam_w_ref = rw["lam"].copy()
+    assert a.device_status() == 0

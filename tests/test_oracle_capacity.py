@@ -104,3 +104,22 @@ def test_no_allowed_configuration_is_an_error():
     inst = queue_instance([0, 2], [[1.0], [2.0]], [0, 0], [5.0])
     with pytest.raises(ValueError):
         oracle.Oracle(inst).effective_capacity(0, [5.0], 0.5)
+
+
+def test_warm_start_converges_faster_on_epoch_market():
+    """On the unit-share epoch market, prices carried over from the previous
+    epoch reach the stop tolerance in far fewer iterations than a cold start
+    (the behaviour the paper reports for warm starts)."""
+    act, que = workloads.epoch_market(4000)
+    pend = workloads.epoch_pending(que.N, 3)
+    qo = oracle.Oracle(que)
+    lam = None
+    for e in range(3):
+        act.capacity = qo.effective_capacity(0, np.full(act.R, 4000.0), 0.5, pend[e])[None]
+        o = oracle.Oracle(act)
+        cold = o.solve(iters=1000, tol=1e-3, trace=False)
+        warm = o.solve(lam0=cold["lam"] if lam is None else lam, iters=1000, tol=1e-3, trace=False)
+        lam = warm["lam"].copy()
+        assert cold["iters_done"][0] < 1000
+        if e > 0:
+            assert warm["iters_done"][0] * 3 < cold["iters_done"][0], (e, warm["iters_done"], cold["iters_done"])

@@ -79,6 +79,7 @@ _S_B, _S_M, _S_S, _S_F, _S_P, _S_Q, _S_CPU, _S_IO = 10, 12, 13, 14, 15, 16, 17, 
 _S_K, _S_TYPE, _S_OFF, _S_STRIDE, _S_BINF, _S_BSAT, _S_W, _S_KV = 20, 21, 22, 23, 24, 25, 26, 27
 _S_G, _S_ETA, _S_TINY_U, _S_TINY_D, _S_TINY_K, _S_TINY_C = 30, 31, 40, 41, 42, 43
 _S_CUR, _S_PEN = 50, 52
+_S_QUEUE = 60
 
 
 @dataclasses.dataclass
@@ -363,6 +364,51 @@ def _ragged(seed: int = 3, n_jobs: int = 1048576) -> Instance:
 
 
 NAMES = ("tiny", "small", "large", "ragged", "batched")
+
+
+# ---------------------------------------------------------------------------
+# Epochs: active jobs + a pending queue, for the warm-start experiment
+# ---------------------------------------------------------------------------
+
+def epoch_market(n_jobs: int = 1048576, queue_frac: float = 0.125, seed: int = 3):
+    """Active jobs and a pending queue for repeated scheduling epochs
+    (Sec. 3.4: C_eff of Eq. 12 at the start of every epoch; Sec. 3.4's
+    complexity paragraph: prices carried over between epochs).
+
+    Both are Ragged-shaped families (generator of the Ragged workload, the
+    queue with its own seed and queue_frac * n_jobs jobs).  Every resource is
+    rescaled so that the active jobs' capacity is n_jobs: one unit per job on
+    average.  Then one step size serves all resources and prices are O(1):
+    eta0 = 2 / n_jobs with the 1/sqrt(t) rule (the Ragged workload's absolute
+    units, 1 to 10^6 per resource, make a single eta overshoot and oscillate).
+    Returns (active, queue)."""
+    act = _ragged(seed, n_jobs)
+    que = _ragged(seed + 1000, max(1, int(round(n_jobs * queue_frac))))
+    scale = float(n_jobs) / act.capacity[0]
+    act.demand = _f32(act.demand.astype(np.float64) * scale[None, None, :])
+    que.demand = _f32(que.demand.astype(np.float64) * scale[None, None, :])
+    R = act.R
+    act.capacity = np.full((1, R), float(n_jobs))
+    que.capacity = act.capacity.copy()
+    act.eta0 = np.array([2.0 / n_jobs])
+    act.rule = STEP_INV_SQRT
+    act.iters = 1000
+    act.name, que.name = "epoch_active", "epoch_queue"
+    return act, que
+
+
+def epoch_pending(n_queue: int, n_epochs: int, seed: int = 3, start: float = 0.5, churn: float = 0.1):
+    """Pending-job masks [n_epochs, n_queue] (uint8): about `start` of the
+    queue is pending in epoch 0; in each later epoch about `churn` of the
+    jobs change state (arrivals and admissions)."""
+    j = np.arange(n_queue, dtype=np.int64)
+    m = (_uniform(seed, _S_QUEUE, j) < start).astype(np.uint8)
+    out = np.empty((n_epochs, n_queue), dtype=np.uint8)
+    for e in range(n_epochs):
+        if e > 0:
+            m = m ^ (_uniform(seed, _S_QUEUE, j + (e * n_queue)) < churn).astype(np.uint8)
+        out[e] = m
+    return out
 
 
 def make(name: str, **kw) -> Instance:
