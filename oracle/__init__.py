@@ -7,8 +7,8 @@ never import it; the two share no code.
 A thin ctypes layer over ``esp_oracle.c`` (plain single-threaded C, fp64,
 ``-ffp-contract=off``), which follows the paper's Sec. 3.2 (Eq. 6-8): per-job
 argmax of utility minus price-weighted demand, exact aggregate demand, and the
-projected-subgradient price update; and Sec. 3.4's effective capacity
-(Eq. 12).
+projected-subgradient price update; Sec. 3.4's effective capacity (Eq. 12);
+and RST's nearest-profile fallback (Sec. 3.1.2).
 """
 from __future__ import annotations
 
@@ -86,6 +86,10 @@ def _declare(L):
     L.orc_solve.restype = C.c_int
     L.orc_effective_capacity.argtypes = [vp, C.c_int, vp, vp, dbl, vp]
     L.orc_effective_capacity.restype = C.c_int
+    L.orc_nearest.argtypes = [vp, C.c_int, i64, vp, vp]
+    L.orc_nearest.restype = i32
+    L.orc_nearest_batch.argtypes = [vp, C.c_int, i64, vp, vp, vp, vp]
+    L.orc_nearest_batch.restype = None
 
 
 def _p(a: Optional[np.ndarray]):
@@ -184,6 +188,24 @@ class Oracle:
         if rc != 0:
             raise ValueError("oracle: a pending job has no allowed configuration")
         return out
+
+    def nearest(self, b: int, family: int, q):
+        """RST nearest-profile fallback for one query: (index within the
+        family or -1, squared l2 distance of the winner)."""
+        q = np.ascontiguousarray(q, dtype=np.float32)
+        d2 = C.c_double(0.0)
+        k = int(self.L.orc_nearest(self._pp, b, int(family), _p(q), C.byref(d2)))
+        return k, float(d2.value)
+
+    def nearest_batch(self, b: int, family, queries):
+        """Batch of queries (family [Q] int32, queries [Q, R] float32):
+        (nearest index [Q] int32, throughput estimate [Q] float32)."""
+        fam = np.ascontiguousarray(family, dtype=np.int32)
+        q = np.ascontiguousarray(queries, dtype=np.float32).reshape(fam.size, self.R)
+        k = np.empty(fam.size, dtype=np.int32)
+        est = np.empty(fam.size, dtype=np.float32)
+        self.L.orc_nearest_batch(self._pp, b, fam.size, _p(fam), _p(q), _p(k), _p(est))
+        return k, est
 
     # whole loop ---------------------------------------------------------
     def solve(self, lam0=None, iters: Optional[int] = None, t_start: int = 1, tol: float = 0.0,

@@ -30,6 +30,10 @@
  *   - the effective capacity of Eq. 12 (Sec. 3.4): the physical capacity
  *     minus gamma times the exact sum, over the pending jobs, of each job's
  *     componentwise smallest demand vector over its family;
+ *   - RST's nearest-profile fallback (Sec. 3.1.2, Sec. 4.1): within a job
+ *     type's profile family, the entry whose resource vector is closest in
+ *     l2 distance to an unprofiled configuration's vector, and its
+ *     throughput as the provisional estimate;
  *   - for the pins only: the Lagrangian dual value g(lambda) of Eq. 6 at the
  *     selected configurations and the primal value sum_j u_{j,c_j} (Eq. 1).
  *
@@ -352,4 +356,57 @@ int orc_effective_capacity(const orc_problem *q, int b, const uint8_t *queued, c
         C_eff[r] = C[r] - g;
     }
     return status;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Nearest-profile interpolation (Sec. 3.1.2 profile fallback, Sec. 4.1).   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For an unprofiled configuration of job type f with resource vector q, the
+ * profile store's entry of the same family whose resource vector is closest
+ * in l2 distance supplies the provisional throughput.  p holds the store
+ * (family f = job type f, utility = profiled throughput, demand = resource
+ * vector).  Squared distance in binary64 in a fixed order,
+ *     e_0 = q_0 - d_0; acc = e_0 * e_0;
+ *     for r = 1..R-1: e_r = q_r - d_r; acc = acc + e_r * e_r,
+ * compared without the square root (monotone); the lowest index wins among
+ * equal distances; entries with feasible == 0 are not candidates.
+ * Returns the index within the family, or -1 when f is out of range or the
+ * family has no allowed entry; *dist2 receives acc of the winner.
+ */
+int32_t orc_nearest(const orc_problem *p, int b, int64_t f, const float *q, double *dist2)
+{
+    const float *d = dem_of(p, b);
+    int64_t e;
+    int32_t best_k = -1;
+    double best = 0.0;
+    if (f < 0 || f >= p->N) return -1;
+    for (e = p->offsets[f]; e < p->offsets[f + 1]; e++) {
+        double acc, x;
+        int r;
+        if (!entry_allowed(p, b, e)) continue;
+        x = (double)q[0] - (double)d[e * p->R];
+        acc = x * x;
+        for (r = 1; r < p->R; r++) {
+            x = (double)q[r] - (double)d[e * p->R + r];
+            acc = acc + x * x;
+        }
+        if (best_k < 0 || acc < best) { best = acc; best_k = (int32_t)(e - p->offsets[f]); }
+    }
+    if (dist2) *dist2 = best;
+    return best_k;
+}
+
+/* A batch of queries of cluster b: family[i], q[i][R] -> k[i] and the
+ * throughput estimate est[i] = utility of the nearest entry (NaN when k < 0). */
+void orc_nearest_batch(const orc_problem *p, int b, int64_t nq, const int32_t *family, const float *q,
+                       int32_t *k, float *est)
+{
+    int64_t i;
+    for (i = 0; i < nq; i++) {
+        int32_t c = orc_nearest(p, b, family[i], q + i * p->R, NULL);
+        k[i] = c;
+        if (est) est[i] = c < 0 ? NAN : util_of(p, b)[p->offsets[family[i]] + c];
+    }
 }

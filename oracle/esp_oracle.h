@@ -41,4 +41,7 @@ int orc_solve(const orc_problem *p, double *lam, int32_t T, int32_t t_start, dou
               double *tr_primal, int32_t *choice_out, double *U_out, int32_t *iters_done);
 int orc_effective_capacity(const orc_problem *q, int b, const uint8_t *queued, const double *C,
                            double gamma, double *C_eff);
+int32_t orc_nearest(const orc_problem *p, int b, int64_t f, const float *q, double *dist2);
+void orc_nearest_batch(const orc_problem *p, int b, int64_t nq, const int32_t *family, const float *q,
+                       int32_t *k, float *est);
 #endif

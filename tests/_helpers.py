@@ -25,8 +25,9 @@ def read_golden(name: str) -> dict:
             if not ln:
                 continue
             key, _, rest = ln.partition(" ")
-            if key == "case":
-                out.setdefault("cases", []).append([[float(x) for x in g.split()] for g in rest.split("|")])
+            if key in ("case", "query", "masked_query"):
+                out.setdefault(key + "s" if key != "case" else "cases", []).append(
+                    [[float(x) for x in g.split()] for g in rest.split("|")])
             elif key == "trace":
                 out["trace"].append([[float(x) for x in g.split()] for g in rest.split("|")])
             elif "|" in rest:
@@ -164,3 +165,21 @@ def brute_effective_capacity(inst, b, capacity, gamma, queued=None) -> np.ndarra
             S += min(vals)
         out[r] = float(capacity[r]) - float(gamma) * float(S)
     return out
+
+
+def store_instance(offsets, utility, demand, feasible=None) -> workloads.Instance:
+    """An instance used as a profile store: family f = job type f, utility =
+    profiled throughput, demand = resource vector."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    nnz = int(offsets[-1])
+    dem = np.asarray(demand, dtype=np.float32).reshape(1, nnz, -1)
+    R = dem.shape[2]
+    inst = workloads.Instance("store", 0, offsets, np.asarray(utility, np.float32).reshape(1, nnz), dem,
+                              np.zeros((1, R)), np.array([0.1]), workloads.STEP_CONST, np.zeros((1, R)), 1)
+    if feasible is not None:
+        inst.feasible = np.asarray(feasible, dtype=np.uint8).reshape(1, nnz)
+    return inst
+
+
+def exact_sq_dist(q, v) -> Fraction:
+    return sum((Fraction(float(a)) - Fraction(float(b))) ** 2 for a, b in zip(q, v))

@@ -12,8 +12,8 @@ import numpy as np
 
 import oracle
 import workloads
-from tests._helpers import (brute_effective_capacity, exact_score, golden_instance, lp_optimum, queue_instance,
-                           read_golden)
+from tests._helpers import (brute_effective_capacity, exact_score, exact_sq_dist, golden_instance, lp_optimum,
+                           queue_instance, read_golden, store_instance)
 
 
 def battery(L) -> None:
@@ -73,6 +73,26 @@ def battery(L) -> None:
     pend = (rng.random(30) < 0.6).astype(np.uint8)
     got = oracle.Oracle(q, L).effective_capacity(0, q.capacity[0], 0.3, pend)
     assert np.array_equal(got, brute_effective_capacity(q, 0, q.capacity[0], 0.3, pend))
+    # nearest-profile fallback: hand example (with and without a masked entry)
+    # and exact-rational optimality on a random store
+    g = read_golden("hand_nearest.txt")
+    for mask, key in ((None, "querys"), (g["masked"], "masked_querys")):
+        o = oracle.Oracle(store_instance(g["offsets"], g["utility"], g["demand"], mask), L)
+        for fam, qv, k, est in g[key]:
+            kk, ee = o.nearest_batch(0, [int(fam[0])], [qv])
+            assert kk[0] == int(k[0])
+            assert (math.isnan(ee[0]) and math.isnan(est[0])) or ee[0] == est[0]
+    rng = np.random.default_rng(11)
+    sizes = rng.integers(1, 12, 25)
+    off = np.concatenate([[0], np.cumsum(sizes)])
+    dem = (rng.random((int(off[-1]), 4)) * np.exp2(rng.integers(-8, 8, 4))).astype(np.float32)
+    o = oracle.Oracle(store_instance(off, rng.random(int(off[-1])), dem), L)
+    for _ in range(100):
+        f = int(rng.integers(0, 25))
+        qv = (rng.random(4) * np.exp2(rng.integers(-8, 8, 4))).astype(np.float32)
+        k = o.nearest(0, f, qv)[0]
+        ex = [exact_sq_dist(qv, dem[e]) for e in range(off[f], off[f + 1])]
+        assert ex[k] <= min(ex) * (1 + 2.0 ** -40)
 
 
 def main(path: str) -> int:

@@ -44,6 +44,14 @@ MUTANTS = {
     "ceff_queue_ignored": ("if (queued != NULL && queued[j] == 0) continue;", ";"),
     "ceff_mask_ignored": ("if (!entry_allowed(q, b, e)) continue;", ";"),
     "ceff_first_config": ("v = d[e * q->R + r];", "v = d[q->offsets[j] * q->R + r];"),
+    "nn_abs_not_square": ("acc = x * x;", "acc = fabs(x);"),
+    "nn_drops_last_dim": ("for (r = 1; r < p->R; r++) {\n            x = (double)q[r]",
+                          "for (r = 1; r + 1 < p->R; r++) {\n            x = (double)q[r]"),
+    "nn_ties_highest": ("if (best_k < 0 || acc < best)", "if (best_k < 0 || acc <= best)"),
+    "nn_mask_ignored": ("if (!entry_allowed(p, b, e)) continue;\n        x = (double)q[0]",
+                        "x = (double)q[0]"),
+    "nn_wrong_dim": ("x = (double)q[r] - (double)d[e * p->R + r];", "x = (double)q[r] - (double)d[e * p->R];"),
+    "nn_estimate_first": ("util_of(p, b)[p->offsets[family[i]] + c]", "util_of(p, b)[p->offsets[family[i]]]"),
     "ceff_whole_config": ("if (!have || v < m) { m = v; have = 1; }",
                           "if (!have || d[e * q->R] < d[(q->offsets[j]) * q->R]) { m = v; have = 1; }"),
 }
