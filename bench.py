@@ -50,6 +50,9 @@ def _parse():
                     help="instead of the default line: E scheduling epochs of an active market plus a pending "
                          "queue (C_eff of Eq. 12 each epoch, then esp_solve to tol 1e-3 from cold and from "
                          "warm prices); prints iterations to converge and epoch times")
+    ap.add_argument("--nearest", type=int, default=0, metavar="Q",
+                    help="instead of the default line: Q nearest-profile queries (RST fallback) against the "
+                         "Ragged table used as the profile store; prints queries/s and the gather roofline")
     ap.add_argument("--epoch-jobs", type=int, default=1048576, help="active jobs of the --epochs market")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic_large.json"),
                     help="HBM bytes per launch measured with rocprofv3 counters, if present")
@@ -106,6 +109,8 @@ def main() -> int:
 
     if args.epochs:
         return _epochs(args, esp, workloads, np, torch)
+    if args.nearest:
+        return _nearest(args, esp, workloads, np, torch)
 
     t_gen = time.perf_counter()
     kw = {}
@@ -262,6 +267,52 @@ def _epochs(args, esp, workloads, np, torch) -> int:
     print(json.dumps(out), flush=True)
     a.close()
     q.close()
+    return 0
+
+
+def _nearest(args, esp, workloads, np, torch) -> int:
+    """RST's nearest-profile fallback (Sec. 3.1.2): Q queries, each naming a
+    job type of the Ragged table (the profile store) and a perturbed resource
+    vector; one esp_nearest_profile call per step, timed with HIP events."""
+    store = workloads.make("ragged")
+    fam_np, q_np = workloads.nn_queries(store, args.nearest, seed=9)
+    fam = torch.from_numpy(fam_np).cuda()
+    q = torch.from_numpy(q_np).cuda()
+    s = esp.Solver(store)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup)):
+            s.nearest_profile(fam, q, stream=stream)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        e0.record(stream)
+        for _ in range(args.steps):
+            s.nearest_profile(fam, q, stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    assert s.device_status() == 0
+    sec = e0.elapsed_time(e1) / 1e3
+    Q, R = args.nearest, store.R
+    sizes = (store.offsets[1:] - store.offsets[:-1])[fam_np[0]]
+    # algorithmic bytes: family id, query vector, family slot (8 B), the
+    # family's utility and R demand columns, and the two outputs
+    bytes_per_call = int(Q * (4 + 4 * R + 8 + 8) + 4 * (1 + R) * int(sizes.sum()))
+    per_call = sec / args.steps
+    out = {
+        "metric": "nearest-profile queries/sec (RST fallback, l2 within the job type's family)",
+        "value": Q / per_call, "unit": "queries/s", "higher_is_better": True,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "f64", "data": "synthetic",
+        "config": {"workload": f"store: Ragged table ({store.N} job types, {store.nnz} profiles, R={R}); "
+                               f"{Q} queries, uniform job type, log-normal(0.25) perturbation, 10% exact hits"},
+        "ms_per_step": per_call * 1e3,
+        "roofline": {"bound": "hbm", "achieved": bytes_per_call / per_call / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": bytes_per_call / per_call / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "k_nearest", "bytes_per_launch": bytes_per_call,
+                     "avg_launch_us": per_call * 1e6},
+    }
+    print(json.dumps(out), flush=True)
+    s.close()
     return 0
 
 

@@ -245,6 +245,34 @@ esp_status esp_effective_capacity(esp_ctx *ctx, esp_ctx *queue, const uint8_t *q
                                   double *capacity_eff, void *stream);
 
 /*
+ * esp_nearest_profile (RST's profile fallback, Sec. 3.1.2 and Sec. 4.1): a
+ * configuration with no profile takes the throughput of the profile-store
+ * entry of its job type whose resource vector is closest in l2 distance.
+ * `store` is a context packed (esp_create) from the profile store: family f
+ * = job type f, utility = profiled throughput T_j(c), demand = resource
+ * vector R_j(c); masked entries (feasible = 0) are not candidates.  For each
+ * of the B x num_queries queries (cluster b's queries search cluster b's
+ * store):
+ *   family    device [B][num_queries] int32, job type of the query;
+ *   query     device [B][num_queries][R] float, the configuration's resource
+ *             vector (finite);
+ *   nearest   device [B][num_queries] int32 out: index within the family of
+ *             the nearest entry (squared distance in binary64, order
+ *             e_0 = q_0 - d_0, acc = e_0 e_0, acc = acc + e_r e_r for
+ *             r = 1..R-1, lowest index among equal distances);
+ *   estimate  device [B][num_queries] float out, or NULL: that entry's
+ *             utility (the provisional throughput).
+ * A family index out of [0, N) or a non-finite query component gives
+ * nearest = -1 and estimate NaN for that query and is reported by
+ * esp_device_status (ESP_ERR_INVALID_ARG / ESP_ERR_NONFINITE).
+ * Stream-ordered and asynchronous; the store may serve any number of calls.
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG (negative count, NULL family,
+ * query or nearest), ESP_ERR_DEVICE.
+ */
+esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_t *family, const float *query,
+                               int32_t *nearest, float *estimate, void *stream);
+
+/*
  * esp_loop_driver: the loop driver esp_solve uses for this context's solves
  * with tol = 0, ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO
  * resolved against the table size, and against the device once a solve has

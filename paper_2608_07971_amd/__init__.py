@@ -81,6 +81,8 @@ _SIGS = {
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
     "esp_loop_driver": ([C.c_void_p, C.POINTER(C.c_int32)], C.c_int),
     "esp_set_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_nearest_profile": ([C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p],
+                            C.c_int),
     "esp_effective_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_double, C.c_void_p, C.c_void_p],
                                C.c_int),
     "esp_destroy": ([C.c_void_p], C.c_int),
@@ -237,6 +239,11 @@ def esp_effective_capacity(ctx: int, queue: Optional[int], queued, gamma: float,
                                         _stream(stream)), "esp_effective_capacity")
 
 
+def esp_nearest_profile(store: int, num_queries: int, family, query, nearest, estimate=None, stream=None) -> None:
+    _check(lib().esp_nearest_profile(store, int(num_queries), _ptr(family), _ptr(query), _ptr(nearest),
+                                     _ptr(estimate), _stream(stream)), "esp_nearest_profile")
+
+
 def esp_destroy(ctx: int) -> None:
     _check(lib().esp_destroy(ctx), "esp_destroy")
 
@@ -319,6 +326,20 @@ class Solver:
 
     def device_status(self, stream=None) -> int:
         return esp_device_status(self.ctx, stream)
+
+    def nearest_profile(self, family, query, stream=None):
+        """RST fallback with this context as the profile store: family
+        int32 [B, Q] and query float32 [B, Q, R] device tensors -> (nearest
+        int32 [B, Q], estimate float32 [B, Q])."""
+        assert family.dtype == torch.int32 and query.dtype == torch.float32
+        assert family.is_contiguous() and query.is_contiguous()
+        assert family.dim() == 2 and family.shape[0] == self.B
+        Q = family.shape[1]
+        assert tuple(query.shape) == (self.B, Q, self.R)
+        nearest = torch.empty((self.B, Q), dtype=torch.int32, device=self.device)
+        est = torch.empty((self.B, Q), dtype=torch.float32, device=self.device)
+        esp_nearest_profile(self.ctx, Q, family, query, nearest, est, stream)
+        return nearest, est
 
     def loop_driver(self) -> int:
         return esp_loop_driver(self.ctx)

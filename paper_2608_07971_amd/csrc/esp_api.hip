@@ -748,6 +748,23 @@ esp_status esp_effective_capacity(esp_ctx *c, esp_ctx *queue, const uint8_t *que
     return dev(launch_reserve(R, queue->base, ra, B, s));
 }
 
+esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_t *family, const float *query,
+                               int32_t *nearest, float *estimate, void *stream) {
+    esp_status st = check_ctx(store);
+    if (st != ESP_OK) return st;
+    if (num_queries < 0) return ESP_ERR_INVALID_ARG;
+    if (num_queries == 0) return ESP_OK;
+    if (family == nullptr || query == nullptr || nearest == nullptr) return ESP_ERR_INVALID_ARG;
+    NearestArgs na;
+    na.family = family;
+    na.query = query;
+    na.nearest = nearest;
+    na.estimate = estimate;
+    na.total = static_cast<int64_t>(store->pl.B) * num_queries;
+    na.Q = num_queries;
+    return dev(launch_nearest(store->pl.R, store->base, na, static_cast<hipStream_t>(stream)));
+}
+
 esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {
     esp_status st = check_ctx(c);
     if (st != ESP_OK) return st;

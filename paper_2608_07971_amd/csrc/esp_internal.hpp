@@ -110,6 +110,18 @@ hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStr
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
+// Arguments of the nearest-profile kernel (RST fallback): queries against
+// the families of a store context (its KArgs supply the table).
+struct NearestArgs {
+    const int32_t *family;         // [B][Q] job type (family index) of each query
+    const float *query;            // [B][Q][R] resource vectors
+    int32_t *nearest;              // [B][Q] index within the family, -1 on error
+    float *estimate;               // [B][Q] utility (throughput) of the nearest entry, or NULL
+    int64_t total;                 // B * Q
+    int32_t Q;                     // queries per cluster
+};
+
+hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStream_t s);
 hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,

@@ -941,6 +941,77 @@ __global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs 
 }
 
 // ---------------------------------------------------------------------------
+// Nearest-profile fallback of RST (Sec. 3.1.2, Sec. 4.1)
+// ---------------------------------------------------------------------------
+
+constexpr int kNearestLanes = 16;                     // lanes per query (one DPP row)
+
+// Query i of a cluster names a job type f and an unprofiled configuration's
+// resource vector q.  The 16 lanes of one DPP row serve one query: lane s
+// takes entries s, s+16, ... of family f, skips masked ones (utility -inf),
+// and keeps the smallest squared l2 distance, computed in binary64 in a fixed
+// order (e_0 = q_0 - d_0, acc = e_0 e_0, acc = acc + e_r e_r for r = 1..R-1).
+// The row then takes the argmax of the negated distance with lowest-index
+// ties (group_argmax), i.e. the nearest entry with the lowest index among
+// equals; lane 0 writes its index and its throughput (the utility column).
+// A family index out of range or a non-finite query component gives -1 /
+// NaN and records an error.
+template <int R>
+__global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs na) {
+    constexpr int kPerBlock = kBlockThreads / kNearestLanes;
+    const int sub = threadIdx.x & (kNearestLanes - 1);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kPerBlock;
+    // every lane of a row shares gi, so rows stay whole for the DPP steps
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kPerBlock + threadIdx.x / kNearestLanes; gi < na.total;
+         gi += stride) {
+        const int cl = static_cast<int>(gi / na.Q);
+        const float *col = a.table + cl * a.cluster_stride;
+        const int f = na.family[gi];
+        double q[R];
+        bool ok = f >= 0 && f < a.N;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float v = na.query[gi * R + r];
+            ok = ok && (fabsf(v) <= 3.402823466e38f);     // false for NaN and +-inf
+            q[r] = static_cast<double>(v);
+        }
+        double best = -__builtin_inf();
+        int bk = 0x7fffffff;
+        uint32_t slot = 0;
+        if (ok) {
+            uint32_t size;
+            if (a.K > 0) {
+                slot = static_cast<uint32_t>(f) * static_cast<uint32_t>(a.K);
+                size = static_cast<uint32_t>(a.K);
+            } else {
+                slot = a.jobs[f].slot;
+                size = a.jobs[f].size;
+            }
+            for (uint32_t k = sub; k < size; k += kNearestLanes) {
+                const size_t e = static_cast<size_t>(slot) + k;
+                if (col[e] == -__builtin_inff()) continue;     // masked configuration
+                double x = q[0] - static_cast<double>(col[a.col_len + e]);
+                double acc = x * x;
+#pragma unroll
+                for (int r = 1; r < R; ++r) {
+                    x = q[r] - static_cast<double>(col[(r + 1) * a.col_len + e]);
+                    acc = acc + x * x;
+                }
+                take_better(best, bk, -acc, static_cast<int>(k));
+            }
+        }
+        group_argmax<kNearestLanes>(best, bk);
+        if (sub == 0) {
+            const bool found = ok && bk != 0x7fffffff;
+            na.nearest[gi] = found ? bk : -1;
+            if (na.estimate)
+                na.estimate[gi] = found ? col[static_cast<size_t>(slot) + static_cast<uint32_t>(bk)] : __builtin_nanf("");
+            if (!ok) atomicCAS(a.status, 0, (f >= 0 && f < a.N) ? kStatusNonfinite : kStatusInvalid);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Granular price update (esp_update_prices) and price validation
 // ---------------------------------------------------------------------------
 
@@ -1064,6 +1135,22 @@ static hipError_t launch_gather_r(const KArgs &a, int B, hipStream_t s) {
 
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s) {
 #define CALL(RR) launch_gather_r<RR>(a, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_nearest_r(const KArgs &a, const NearestArgs &na, hipStream_t s) {
+    constexpr int kPerBlock = kBlockThreads / kNearestLanes;
+    const int64_t need = (na.total + kPerBlock - 1) / kPerBlock;
+    const int64_t cap = 256 * 32;                    // enough resident queries to cover gather latency
+    const dim3 grid(static_cast<unsigned>(need < cap ? need : cap)), block(kBlockThreads);
+    hipLaunchKernelGGL((k_nearest<R>), grid, block, 0, s, a, na);
+    return hipGetLastError();
+}
+
+hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStream_t s) {
+#define CALL(RR) launch_nearest_r<RR>(a, na, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }

@@ -80,6 +80,7 @@ _S_K, _S_TYPE, _S_OFF, _S_STRIDE, _S_BINF, _S_BSAT, _S_W, _S_KV = 20, 21, 22, 23
 _S_G, _S_ETA, _S_TINY_U, _S_TINY_D, _S_TINY_K, _S_TINY_C = 30, 31, 40, 41, 42, 43
 _S_CUR, _S_PEN = 50, 52
 _S_QUEUE = 60
+_S_NNF, _S_NNB, _S_NNZ, _S_NNX = 70, 71, 72, 73
 
 
 @dataclasses.dataclass
@@ -409,6 +410,32 @@ def epoch_pending(n_queue: int, n_epochs: int, seed: int = 3, start: float = 0.5
             m = m ^ (_uniform(seed, _S_QUEUE, j + (e * n_queue)) < churn).astype(np.uint8)
         out[e] = m
     return out
+
+
+# ---------------------------------------------------------------------------
+# Queries of the nearest-profile fallback (RST)
+# ---------------------------------------------------------------------------
+
+def nn_queries(store: Instance, n_queries: int, seed: int = 5, exact_frac: float = 0.1, sigma: float = 0.25):
+    """Unprofiled configurations for the profile store `store` (family f =
+    job type f): per query a job type drawn uniformly, a base entry of its
+    family drawn uniformly, and the base's resource vector multiplied per
+    resource by exp(sigma Z) (a knob combination between profiled ones); a
+    fraction exact_frac are exact copies of a profiled vector (store hits).
+    Returns (family int32 [B, Q], query float32 [B, Q, R])."""
+    B, N, R = store.B, store.N, store.R
+    i = np.arange(B * n_queries, dtype=np.int64)
+    fam = np.minimum(np.floor(N * _uniform(seed, _S_NNF, i)).astype(np.int64), N - 1)
+    off = store.offsets
+    size = off[fam + 1] - off[fam]
+    k = np.minimum(np.floor(size * _uniform(seed, _S_NNB, i)).astype(np.int64), size - 1)
+    b = i // n_queries
+    base = store.demand[b, off[fam] + k].astype(np.float64)
+    z = _normal(seed, _S_NNZ, np.arange(B * n_queries * R, dtype=np.int64)).reshape(-1, R)
+    factor = np.exp(sigma * z)
+    factor[_uniform(seed, _S_NNX, i) < exact_frac] = 1.0
+    q = _f32(base * factor)
+    return fam.astype(np.int32).reshape(B, n_queries), q.reshape(B, n_queries, R)
 
 
 def make(name: str, **kw) -> Instance:
