@@ -36,6 +36,19 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+MAX_PER_GPU = 4
+MAX_SHARDS = 8
+
+
+class _Iac(C.Structure):
+    _fields_ = [
+        ("G", C.c_int32), ("gpu_memory", C.c_double), ("gpu_compute", C.c_double),
+        ("r_gpus", C.c_int32), ("r_mem", C.c_int32), ("r_sm", C.c_int32),
+        ("sensitivity", C.c_void_p), ("pressure", C.c_void_p), ("tau_base", C.c_void_p),
+        ("beta", C.c_double), ("beta_max", C.c_double), ("u_target", C.c_double), ("kappa", C.c_double),
+    ]
+
+
 class _Problem(C.Structure):
     _fields_ = [
         ("B", C.c_int32), ("N", C.c_int32), ("R", C.c_int32), ("nnz", C.c_int64),
@@ -86,6 +99,12 @@ def _declare(L):
     L.orc_solve.restype = C.c_int
     L.orc_effective_capacity.argtypes = [vp, C.c_int, vp, vp, dbl, vp]
     L.orc_effective_capacity.restype = C.c_int
+    L.orc_binpack.argtypes = [vp, C.c_int, vp, vp, vp]
+    L.orc_binpack.restype = i64
+    L.orc_iac_eval.argtypes = [vp, C.c_int, vp, vp, vp, vp]
+    L.orc_iac_eval.restype = i64
+    L.orc_schedule.argtypes = [vp, C.c_int, vp, i32, i32, dbl, vp, vp, vp, vp, vp, vp]
+    L.orc_schedule.restype = C.c_int
     L.orc_nearest.argtypes = [vp, C.c_int, i64, vp, vp]
     L.orc_nearest.restype = i32
     L.orc_nearest_batch.argtypes = [vp, C.c_int, i64, vp, vp, vp, vp]
@@ -206,6 +225,53 @@ class Oracle:
         est = np.empty(fam.size, dtype=np.float32)
         self.L.orc_nearest_batch(self._pp, b, fam.size, _p(fam), _p(q), _p(k), _p(est))
         return k, est
+
+    # Alg. 1 outer rounds ---------------------------------------------------
+    def _iac(self, model, b):
+        sa = np.ascontiguousarray(model.sensitivity, dtype=np.float32)
+        pr = np.ascontiguousarray(model.pressure, dtype=np.float32)
+        tb = np.ascontiguousarray(model.tau_base, dtype=np.float64)
+        keep = (sa, pr, tb)
+        m = _Iac(int(model.gpus[b]), float(model.gpu_memory), float(model.gpu_compute), int(model.r_gpus),
+                 int(model.r_mem), int(model.r_sm), _p(sa), _p(pr), _p(tb), float(model.beta),
+                 float(model.beta_max), float(model.u_target), float(model.kappa))
+        return m, keep
+
+    def binpack(self, b: int, model, choice):
+        """First-fit BinPack of cluster b's selection: (occupants [G, 4], shares placed)."""
+        m, keep = self._iac(model, b)
+        ch = np.ascontiguousarray(choice, dtype=np.int32)
+        occ = np.empty((m.G, MAX_PER_GPU), dtype=np.int32)
+        placed = int(self.L.orc_binpack(self._pp, b, C.byref(m), _p(ch), _p(occ)))
+        return occ, placed
+
+    def iac_eval(self, b: int, model, choice, occ):
+        """Co-located pairs against Eq. 11: (violating pairs, largest excess per job [N])."""
+        m, keep = self._iac(model, b)
+        ch = np.ascontiguousarray(choice, dtype=np.int32)
+        oc = np.ascontiguousarray(occ, dtype=np.int32)
+        inc = np.empty(self.N, dtype=np.float64)
+        V = int(self.L.orc_iac_eval(self._pp, b, C.byref(m), _p(ch), _p(oc), _p(inc)))
+        return V, inc
+
+    def schedule(self, b: int, model, rounds: int, iters: int, tol: float = 0.0, lam0=None) -> dict:
+        """Alg. 1 on cluster b: prices, choice, occupants of the last round,
+        rounds run, violating pairs of the last round, final penalties."""
+        m, keep = self._iac(model, b)
+        lam = np.array(self.inst.lam0[b] if lam0 is None else lam0, dtype=np.float64).reshape(self.R).copy()
+        # the instance's interference penalties as the starting Gamma (Alg. 1 resets them)
+        pen = (np.zeros(int(self.offsets[-1]), dtype=np.float32) if self.penalty is None
+               else self.penalty[b].copy())
+        ch = np.empty(self.N, dtype=np.int32)
+        occ = np.empty((m.G, MAX_PER_GPU), dtype=np.int32)
+        nr = C.c_int32(0)
+        nv = C.c_int64(0)
+        rc = self.L.orc_schedule(self._pp, b, C.byref(m), int(rounds), int(iters), float(tol), _p(lam), _p(pen),
+                                 _p(ch), _p(occ), C.byref(nr), C.byref(nv))
+        if rc != 0:
+            raise ValueError(f"oracle: schedule failed (rc={rc})")
+        return {"lam": lam, "penalty": pen, "choice": ch, "occ": occ, "rounds": int(nr.value),
+                "violations": int(nv.value)}
 
     # whole loop ---------------------------------------------------------
     def solve(self, lam0=None, iters: Optional[int] = None, t_start: int = 1, tol: float = 0.0,

@@ -30,6 +30,10 @@
  *   - the effective capacity of Eq. 12 (Sec. 3.4): the physical capacity
  *     minus gamma times the exact sum, over the pending jobs, of each job's
  *     componentwise smallest demand vector over its family;
+ *   - the outer rounds of Alg. 1 (Sec. 3.4): first-fit BinPack of the
+ *     selection onto GPUs, the co-located pairs' predicted slowdowns against
+ *     the thresholds of Eq. 11, and penalty updates for the offending
+ *     configurations, repeated until no pair violates;
  *   - RST's nearest-profile fallback (Sec. 3.1.2, Sec. 4.1): within a job
  *     type's profile family, the entry whose resource vector is closest in
  *     l2 distance to an unprofiled configuration's vector, and its
@@ -409,4 +413,166 @@ void orc_nearest_batch(const orc_problem *p, int b, int64_t nq, const int32_t *f
         k[i] = c;
         if (est) est[i] = c < 0 ? NAN : util_of(p, b)[p->offsets[family[i]] + c];
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Outer ESP-IAC rounds (Sec. 3.4, Alg. 1; thresholds of Eq. 11).           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * BinPack (not specified by the paper; first fit): jobs in index order; job j
+ * at its chosen configuration needs g = d_j[r_gpus] GPUs (a whole number in
+ * 1..ORC_MAX_SHARDS, otherwise the job is not placeable) and on each of them
+ * d_j[r_mem] / g memory and d_j[r_sm] / g compute share.  It takes the g
+ * lowest-index GPUs that have room for one share (memory and compute left,
+ * fewer than ORC_MAX_PER_GPU jobs), all or nothing, and their residuals drop
+ * by one share each.  occ[h * ORC_MAX_PER_GPU + i] lists GPU h's jobs in
+ * placement order (-1 = empty slot).  Returns the number of shares placed.
+ */
+int64_t orc_binpack(const orc_problem *p, int b, const orc_iac *m, const int32_t *choice, int32_t *occ)
+{
+    const float *d = dem_of(p, b);
+    double *mem = (double *)malloc(sizeof(double) * (size_t)m->G);
+    double *sm = (double *)malloc(sizeof(double) * (size_t)m->G);
+    int *cnt = (int *)calloc((size_t)m->G, sizeof(int));
+    int64_t placed = 0, j;
+    int h;
+    if (mem == NULL || sm == NULL || cnt == NULL) { free(mem); free(sm); free(cnt); return -1; }
+    for (h = 0; h < m->G; h++) { mem[h] = m->gpu_memory; sm[h] = m->gpu_compute; }
+    for (h = 0; h < m->G * ORC_MAX_PER_GPU; h++) occ[h] = -1;
+    for (j = 0; j < p->N; j++) {
+        int64_t e;
+        double gv, need_m, need_s;
+        int g, sel[ORC_MAX_SHARDS], found = 0, i;
+        if (choice[j] < 0) continue;
+        e = p->offsets[j] + choice[j];
+        gv = (double)d[e * p->R + m->r_gpus];
+        if (!(gv >= 1.0 && gv <= ORC_MAX_SHARDS && gv == floor(gv))) continue;
+        g = (int)gv;
+        need_m = (double)d[e * p->R + m->r_mem] / gv;
+        need_s = (double)d[e * p->R + m->r_sm] / gv;
+        for (h = 0; h < m->G && found < g; h++)
+            if (cnt[h] < ORC_MAX_PER_GPU && mem[h] >= need_m && sm[h] >= need_s) sel[found++] = h;
+        if (found < g) continue;
+        for (i = 0; i < g; i++) {
+            h = sel[i];
+            mem[h] = mem[h] - need_m;
+            sm[h] = sm[h] - need_s;
+            occ[h * ORC_MAX_PER_GPU + cnt[h]] = (int32_t)j;
+            cnt[h]++;
+        }
+        placed += g;
+    }
+    free(mem); free(sm); free(cnt);
+    return placed;
+}
+
+/*
+ * IacPredict over every co-located pair (Alg. 1): on each GPU, every pair of
+ * its jobs (x placed before y) with predicted slowdowns
+ *     S_x|y = 1 + a_x * b_y,   S_y|x = 1 + a_y * b_x
+ * (a = sensitivity, b = pressure of each job's chosen configuration: a
+ * synthetic stand-in for the trained predictor of Sec. 3.3.2) against the
+ * thresholds of Eq. 11,
+ *     tau_x = tau_base_x + min(beta * (U / U_target - 1), beta_max),
+ * U = (GPUs holding at least one job) / G, the packing's GPU utilisation.  A pair violates
+ * when either slowdown exceeds its threshold; inc[x] receives the largest
+ * excess S_x|y - tau_x of job x over all its pairs (0 if none).  Returns the
+ * number of violating pairs.
+ */
+int64_t orc_iac_eval(const orc_problem *p, int b, const orc_iac *m, const int32_t *choice, const int32_t *occ,
+                     double *inc)
+{
+    const float *sa = m->sensitivity + (int64_t)b * p->nnz;
+    const float *pb = m->pressure + (int64_t)b * p->nnz;
+    const double *tb = m->tau_base + (int64_t)b * p->N;
+    double q, w, add;
+    int64_t V = 0, j, used = 0;
+    int h, x, y;
+    for (j = 0; j < p->N; j++) inc[j] = 0.0;
+    for (h = 0; h < m->G; h++) used += occ[h * ORC_MAX_PER_GPU] >= 0;
+    q = (double)used / (double)m->G;
+    q = q / m->u_target;
+    w = q - 1.0;
+    add = m->beta * w;
+    if (add > m->beta_max) add = m->beta_max;
+    for (h = 0; h < m->G; h++) {
+        const int32_t *o = occ + h * ORC_MAX_PER_GPU;
+        for (x = 0; x < ORC_MAX_PER_GPU; x++) {
+            if (o[x] < 0) break;
+            for (y = x + 1; y < ORC_MAX_PER_GPU; y++) {
+                int32_t jx = o[x], jy = o[y];
+                int64_t ex, ey;
+                double sxy, syx, ox, oy;
+                if (jy < 0) break;
+                ex = p->offsets[jx] + choice[jx];
+                ey = p->offsets[jy] + choice[jy];
+                sxy = (double)sa[ex] * (double)pb[ey];
+                sxy = 1.0 + sxy;
+                syx = (double)sa[ey] * (double)pb[ex];
+                syx = 1.0 + syx;
+                ox = sxy - (tb[jx] + add);
+                oy = syx - (tb[jy] + add);
+                if (ox > 0.0 && ox > inc[jx]) inc[jx] = ox;
+                if (oy > 0.0 && oy > inc[jy]) inc[jy] = oy;
+                if (ox > 0.0 || oy > 0.0) V++;
+            }
+        }
+    }
+    return V;
+}
+
+/*
+ * Alg. 1 for cluster b: Gamma <- 0 (the interference penalties; the switching
+ * cost stays), then for rounds m = 1..M: the tatonnement (T iterations from
+ * the current prices, t = 1.., stop tolerance tol) and the re-selection at
+ * its prices, BinPack, IacPredict over co-located pairs; no violation ends
+ * the loop, otherwise each violating job's chosen configuration has its
+ * penalty raised by kappa times its largest excess,
+ *     Gamma_jc <- (float)(Gamma_jc + kappa * inc_j),
+ * and the next round starts from the prices reached.
+ * penalty: [nnz] of cluster b, in/out; lam [R] in/out; choice [N] and occ
+ * [G * ORC_MAX_PER_GPU] of the last round; *rounds = rounds run, *viol =
+ * violating pairs of the last round.  Returns 0, or -1 on a failed solve.
+ */
+int orc_schedule(const orc_problem *p, int b, const orc_iac *m, int32_t M, int32_t T, double tol, double *lam,
+                 float *penalty, int32_t *choice, int32_t *occ, int32_t *rounds, int64_t *viol)
+{
+    orc_problem v = *p;
+    double *inc = (double *)malloc(sizeof(double) * (size_t)(p->N > 0 ? p->N : 1));
+    int32_t r;
+    int64_t j, e;
+    if (inc == NULL) return -2;
+    /* a one-cluster view of cluster b whose penalty is the working copy */
+    v.B = 1;
+    v.utility = p->utility + (int64_t)b * p->nnz;
+    v.demand = p->demand + (int64_t)b * p->nnz * p->R;
+    v.feasible = p->feasible ? p->feasible + (int64_t)b * p->nnz : NULL;
+    v.capacity = p->capacity + (int64_t)b * p->R;
+    v.eta0 = p->eta0 + b;
+    v.current = p->current ? p->current + (int64_t)b * p->N : NULL;
+    v.switch_cost = p->switch_cost ? p->switch_cost + b : NULL;
+    v.penalty = penalty;
+    for (e = 0; e < p->nnz; e++) penalty[e] = 0.0f;
+    *rounds = 0;
+    *viol = 0;
+    for (r = 1; r <= M; r++) {
+        int64_t V;
+        if (orc_solve(&v, lam, T, 1, tol, NULL, NULL, NULL, NULL, NULL, choice, NULL, NULL) != 0) {
+            free(inc);
+            return -1;
+        }
+        if (orc_binpack(&v, 0, m, choice, occ) < 0) { free(inc); return -2; }
+        V = orc_iac_eval(p, b, m, choice, occ, inc);
+        *rounds = r;
+        *viol = V;
+        if (V == 0) break;
+        for (j = 0; j < p->N; j++)
+            if (inc[j] > 0.0) {
+                e = p->offsets[j] + choice[j];
+                penalty[e] = (float)((double)penalty[e] + m->kappa * inc[j]);
+            }
+    }
+    free(inc);
+    return 0;
 }

@@ -44,4 +44,23 @@ int orc_effective_capacity(const orc_problem *q, int b, const uint8_t *queued, c
 int32_t orc_nearest(const orc_problem *p, int b, int64_t f, const float *q, double *dist2);
 void orc_nearest_batch(const orc_problem *p, int b, int64_t nq, const int32_t *family, const float *q,
                        int32_t *k, float *est);
+
+/* Alg. 1 outer rounds: cluster model and synthetic interference inputs. */
+#define ORC_MAX_PER_GPU 4
+#define ORC_MAX_SHARDS 8
+typedef struct {
+    int32_t G;                /* GPUs of the cluster */
+    double gpu_memory;        /* per-GPU capacity of resource r_mem */
+    double gpu_compute;       /* per-GPU capacity of resource r_sm */
+    int32_t r_gpus, r_mem, r_sm;
+    const float *sensitivity; /* [B][nnz] a of each configuration */
+    const float *pressure;    /* [B][nnz] b of each configuration */
+    const double *tau_base;   /* [B][N] */
+    double beta, beta_max, u_target, kappa;
+} orc_iac;
+int64_t orc_binpack(const orc_problem *p, int b, const orc_iac *m, const int32_t *choice, int32_t *occ);
+int64_t orc_iac_eval(const orc_problem *p, int b, const orc_iac *m, const int32_t *choice, const int32_t *occ,
+                     double *inc);
+int orc_schedule(const orc_problem *p, int b, const orc_iac *m, int32_t M, int32_t T, double tol, double *lam,
+                 float *penalty, int32_t *choice, int32_t *occ, int32_t *rounds, int64_t *viol);
 #endif

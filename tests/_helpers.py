@@ -25,7 +25,7 @@ def read_golden(name: str) -> dict:
             if not ln:
                 continue
             key, _, rest = ln.partition(" ")
-            if key in ("case", "query", "masked_query"):
+            if key in ("case", "query", "masked_query", "result"):
                 out.setdefault(key + "s" if key != "case" else "cases", []).append(
                     [[float(x) for x in g.split()] for g in rest.split("|")])
             elif key == "trace":
@@ -183,3 +183,56 @@ def store_instance(offsets, utility, demand, feasible=None) -> workloads.Instanc
 
 def exact_sq_dist(q, v) -> Fraction:
     return sum((Fraction(float(a)) - Fraction(float(b))) ** 2 for a, b in zip(q, v))
+
+
+def schedule_fixture(name: str = "hand_schedule.txt"):
+    """The instance, the IAC model and the expected results of a hand-derived
+    Alg. 1 fixture."""
+    g = read_golden(name)
+    inst = golden_instance(g)
+    B, nnz, N = 1, inst.nnz, inst.N
+    m = workloads.IacModel(np.array([int(g["gpus"][0])], np.int32), g["gpu_memory"][0], g["gpu_compute"][0],
+                           *[int(x) for x in g["resources"]],
+                           np.array(g["sensitivity"], np.float32).reshape(B, nnz),
+                           np.array(g["pressure"], np.float32).reshape(B, nnz),
+                           np.array(g["tau_base"], np.float64).reshape(B, N),
+                           g["beta"][0], g["beta_max"][0], g["u_target"][0], g["kappa"][0])
+    return inst, m, g["results"]
+
+
+def check_first_fit(inst, b, model, choice, occ):
+    """Checks that occ is the first-fit packing of the selection: capacities
+    respected, and replaying the jobs in index order, each job sits on the
+    first g GPUs that had room, or is absent when fewer than g had room."""
+    G = int(model.gpus[b])
+    mem = [float(model.gpu_memory)] * G
+    sm = [float(model.gpu_compute)] * G
+    cnt = [0] * G
+    where = {}
+    for h in range(G):
+        for i, j in enumerate(occ[h]):
+            if j >= 0:
+                where.setdefault(int(j), []).append((h, i))
+    for j in range(inst.N):
+        e = inst.offsets[j] + choice[j]
+        gv = float(inst.demand[b, e, model.r_gpus])
+        placeable = 1.0 <= gv <= 8.0 and gv == int(gv)
+        if not placeable:
+            assert j not in where
+            continue
+        g = int(gv)
+        nm = float(inst.demand[b, e, model.r_mem]) / gv
+        ns = float(inst.demand[b, e, model.r_sm]) / gv
+        room = [h for h in range(G) if cnt[h] < 4 and mem[h] >= nm and sm[h] >= ns]
+        if len(room) < g:
+            assert j not in where, j
+            continue
+        got = sorted(h for h, _ in where[j])
+        assert got == room[:g], (j, got, room[:g])
+        for h, i in where[j]:
+            assert i == cnt[h]                      # placement order on the GPU
+            mem[h] -= nm
+            sm[h] -= ns
+            cnt[h] += 1
+    for h in range(G):
+        assert all(x == -1 for x in occ[h][cnt[h]:])

@@ -12,8 +12,8 @@ import numpy as np
 
 import oracle
 import workloads
-from tests._helpers import (brute_effective_capacity, exact_score, exact_sq_dist, golden_instance, lp_optimum,
-                           queue_instance, read_golden, store_instance)
+from tests._helpers import (brute_effective_capacity, check_first_fit, exact_score, exact_sq_dist, golden_instance,
+                           lp_optimum, queue_instance, read_golden, schedule_fixture, store_instance)
 
 
 def battery(L) -> None:
@@ -93,6 +93,40 @@ def battery(L) -> None:
         k = o.nearest(0, f, qv)[0]
         ex = [exact_sq_dist(qv, dem[e]) for e in range(off[f], off[f + 1])]
         assert ex[k] <= min(ex) * (1 + 2.0 ** -40)
+    # outer rounds of Alg. 1: hand example, first fit, pairs and penalties
+    inst, m, results = schedule_fixture()
+    inst.penalty = np.array([[0.5, 2.0, 1.0, 0.25]], np.float32)      # reset by Alg. 1's first step
+    o = oracle.Oracle(inst, L)
+    for M, nr, V, ch, g0, g1, pen in results:
+        r = o.schedule(0, m, int(M[0]), inst.iters)
+        assert r["rounds"] == int(nr[0]) and r["violations"] == int(V[0])
+        assert list(r["choice"]) == [int(x) for x in ch]
+        assert list(r["occ"][0]) == [int(x) for x in g0] and list(r["occ"][1]) == [int(x) for x in g1]
+        assert list(r["penalty"]) == pen
+    inst = workloads.make("small", n_jobs=600)
+    m = workloads.iac_model(inst)
+    o = oracle.Oracle(inst, L)
+    ch = o.select(0, np.full(inst.R, 0.05))
+    occ, _ = o.binpack(0, m, ch)
+    check_first_fit(inst, 0, m, ch, occ)
+    from tests.test_oracle_schedule import _exact_pairs
+    r1 = o.schedule(0, m, 1, 40)
+    ch, occ = r1["choice"], r1["occ"]
+    check_first_fit(inst, 0, m, ch, occ)
+    V, inc = o.iac_eval(0, m, ch, occ)
+    Vx, incx = _exact_pairs(inst, 0, m, ch, occ)
+    assert V == Vx and V > 0
+    for j in range(inst.N):
+        assert abs(inc[j] - float(incx.get(j, 0))) <= 1e-14
+    r2 = o.schedule(0, m, 2, 40)
+    assert r1["violations"] == V
+    if r1["violations"]:
+        V1, inc1 = o.iac_eval(0, m, r1["choice"], r1["occ"])
+        for j in range(inst.N):
+            e = inst.offsets[j] + r1["choice"][j]
+            want = np.float32(m.kappa * inc1[j]) if inc1[j] > 0 else np.float32(0)
+            assert r1["penalty"][e] == want
+        assert r2["rounds"] == 2
 
 
 def main(path: str) -> int:

@@ -44,6 +44,16 @@ MUTANTS = {
     "ceff_queue_ignored": ("if (queued != NULL && queued[j] == 0) continue;", ";"),
     "ceff_mask_ignored": ("if (!entry_allowed(q, b, e)) continue;", ";"),
     "ceff_first_config": ("v = d[e * q->R + r];", "v = d[q->offsets[j] * q->R + r];"),
+    "bp_last_fit": ("for (h = 0; h < m->G && found < g; h++)", "for (h = m->G - 1; h >= 0 && found < g; h--)"),
+    "bp_ignores_compute": ("mem[h] >= need_m && sm[h] >= need_s", "mem[h] >= need_m"),
+    "bp_share_not_divided": ("need_m = (double)d[e * p->R + m->r_mem] / gv;", "need_m = (double)d[e * p->R + m->r_mem];"),
+    "iac_wrong_pressure": ("sxy = (double)sa[ex] * (double)pb[ey];", "sxy = (double)sa[ex] * (double)pb[ex];"),
+    "iac_no_clamp": ("if (add > m->beta_max) add = m->beta_max;", ";"),
+    "iac_and_not_or": ("if (ox > 0.0 || oy > 0.0) V++;", "if (ox > 0.0 && oy > 0.0) V++;"),
+    "gamma_not_reset": ("for (e = 0; e < p->nnz; e++) penalty[e] = 0.0f;", ";"),
+    "penalty_no_kappa": ("penalty[e] = (float)((double)penalty[e] + m->kappa * inc[j]);",
+                         "penalty[e] = (float)((double)penalty[e] + inc[j]);"),
+    "rounds_no_break": ("if (V == 0) break;", ";"),
     "nn_abs_not_square": ("acc = x * x;", "acc = fabs(x);"),
     "nn_drops_last_dim": ("for (r = 1; r < p->R; r++) {\n            x = (double)q[r]",
                           "for (r = 1; r + 1 < p->R; r++) {\n            x = (double)q[r]"),

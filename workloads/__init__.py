@@ -81,6 +81,7 @@ _S_G, _S_ETA, _S_TINY_U, _S_TINY_D, _S_TINY_K, _S_TINY_C = 30, 31, 40, 41, 42, 4
 _S_CUR, _S_PEN = 50, 52
 _S_QUEUE = 60
 _S_NNF, _S_NNB, _S_NNZ, _S_NNX = 70, 71, 72, 73
+_S_IA, _S_IB, _S_IT = 80, 81, 82
 
 
 @dataclasses.dataclass
@@ -410,6 +411,50 @@ def epoch_pending(n_queue: int, n_epochs: int, seed: int = 3, start: float = 0.5
             m = m ^ (_uniform(seed, _S_QUEUE, j + (e * n_queue)) < churn).astype(np.uint8)
         out[e] = m
     return out
+
+
+# ---------------------------------------------------------------------------
+# Outer ESP-IAC rounds (Alg. 1): cluster model and synthetic slowdown inputs
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class IacModel:
+    """GPU-level cluster model for BinPack and the inputs of the predicted
+    slowdown S_x|y = 1 + a_x b_y of a co-located pair (a synthetic stand-in
+    for the trained predictor of Sec. 3.3.2), with the Eq. 11 thresholds."""
+    gpus: np.ndarray              # int32 [B] GPUs per cluster
+    gpu_memory: float             # per-GPU capacity of resource r_mem
+    gpu_compute: float            # per-GPU capacity of resource r_sm
+    r_gpus: int                   # resource holding the GPU count (whole numbers)
+    r_mem: int
+    r_sm: int
+    sensitivity: np.ndarray       # float32 [B, nnz] a: how much a configuration suffers
+    pressure: np.ndarray          # float32 [B, nnz] b: how much it disturbs its neighbour
+    tau_base: np.ndarray          # float64 [B, N] baseline tolerance
+    beta: float = 0.5
+    beta_max: float = 0.1
+    u_target: float = 0.8
+    kappa: float = 0.5
+
+
+def iac_model(inst: Instance, seed: int = 11, gpus=None, gpu_memory: float = 80.0,
+              gpu_compute: float = 1.0) -> IacModel:
+    """Synthetic interference inputs for `inst` (resources 0, 1, 2 = GPU
+    count, GPU memory, compute share, as in every workload here):
+    sensitivity a ~ U[0, 0.6) per configuration; pressure b = (compute share
+    per GPU) x U[0.5, 1); tau_base ~ U[1.1, 1.4) per job; GPUs per cluster =
+    the capacity's GPU count unless given."""
+    B, N, nnz = inst.B, inst.N, inst.nnz
+    e = np.arange(B * nnz, dtype=np.int64)
+    a = 0.6 * _uniform(seed, _S_IA, e)
+    d = inst.demand.reshape(B * nnz, inst.R).astype(np.float64)
+    share = d[:, 2] / np.maximum(d[:, 0], 1.0)
+    bb = share * (0.5 + 0.5 * _uniform(seed, _S_IB, e))
+    tb = 1.1 + 0.3 * _uniform(seed, _S_IT, np.arange(B * N, dtype=np.int64))
+    if gpus is None:
+        gpus = np.rint(inst.capacity[:, 0]).astype(np.int32)
+    return IacModel(np.asarray(gpus, dtype=np.int32).reshape(B), gpu_memory, gpu_compute, 0, 1, 2,
+                    _f32(a).reshape(B, nnz), _f32(bb).reshape(B, nnz), tb.reshape(B, N))
 
 
 # ---------------------------------------------------------------------------
