@@ -245,6 +245,77 @@ esp_status esp_effective_capacity(esp_ctx *ctx, esp_ctx *queue, const uint8_t *q
                                   double *capacity_eff, void *stream);
 
 /*
+ * Outer ESP-IAC rounds (Sec. 3.4, Alg. 1).  GPU-level cluster model for the
+ * BinPack step and the inputs of the predicted slowdown of a co-located
+ * pair, S_x|y = 1 + a_x b_y (a: sensitivity, b: pressure of each job's
+ * chosen configuration), a stand-in for the trained predictor of Sec. 3.3.2,
+ * with the adaptive thresholds of Eq. 11.
+ */
+#define ESP_MAX_GPUS 2048      /* GPUs per cluster */
+#define ESP_MAX_PER_GPU 4      /* jobs sharing one GPU */
+typedef struct {
+    const int32_t *gpus;       /* host [B]: GPUs of each cluster, 1..ESP_MAX_GPUS */
+    double gpu_memory;         /* per-GPU capacity of resource r_mem (>= 0) */
+    double gpu_compute;        /* per-GPU capacity of resource r_sm (>= 0) */
+    int32_t r_gpus;            /* resource holding a configuration's GPU count (1..8 whole GPUs;
+                                  other values: the job is not placeable) */
+    int32_t r_mem;             /* resource split evenly over the job's GPUs: memory */
+    int32_t r_sm;              /* resource split evenly over the job's GPUs: compute share */
+    const float *sensitivity;  /* device [B][nnz] a per configuration (entry order of esp_problem) */
+    const float *pressure;     /* device [B][nnz] b per configuration */
+    const double *tau_base;    /* device [B][N] baseline tolerance of each job */
+    double beta;               /* Eq. 11 sensitivity to utilisation */
+    double beta_max;           /* Eq. 11 clamp of the additive term */
+    double u_target;           /* Eq. 11 utilisation target (> 0) */
+    double kappa;              /* penalty per unit of excess slowdown (>= 0) */
+} esp_iac_model;
+
+/*
+ * esp_schedule (Alg. 1): Gamma <- 0 (the interference penalties of the
+ * context's penalty column; switching costs stay), then rounds m = 1..
+ * max_rounds, per cluster:
+ *   1. the tatonnement: esp_solve from `prices` (t = 1.., `iters`, `tol`),
+ *      the selection c* at the prices reached written to `choice`;
+ *   2. BinPack (first fit; the paper names no algorithm): jobs in index
+ *      order; job j needs g = d_j[r_gpus] GPUs and d_j[r_mem] / g memory and
+ *      d_j[r_sm] / g compute on each; it takes the g lowest-index GPUs with
+ *      room for one share and fewer than ESP_MAX_PER_GPU jobs, all or
+ *      nothing (binary64 residuals, updated in job order);
+ *   3. IacPredict on every pair (x, y) sharing a GPU: the pair violates when
+ *      S_x|y > tau_x or S_y|x > tau_y, tau_x = tau_base_x + min(beta (U /
+ *      u_target - 1), beta_max), U = busy GPUs / G;
+ *   4. no violation: the cluster's schedule is final (later rounds leave it
+ *      alone); otherwise each violating job's chosen configuration has its
+ *      penalty raised by kappa times its largest excess S - tau (binary64,
+ *      rounded once to fp32), and the next round starts from the prices
+ *      reached.
+ * Outputs (device): prices [B][R] of each cluster's last round; choice
+ * [B][N]; gpu_jobs [B][max gpus][ESP_MAX_PER_GPU], GPU h's jobs in placement
+ * order, -1 for an empty slot; rounds_used [B]; violations [B], the
+ * violating pairs of the last round.  The context's penalty column keeps the
+ * final Gamma.  The context must have been created with penalty inputs
+ * (esp_problem.current / switch_cost / penalty).  Synchronises `stream` once
+ * per round (to stop when every cluster is free of violations).
+ * Errors: ESP_ERR_STATE (NULL context or no penalty column),
+ * ESP_ERR_INVALID_ARG (NULL pointers, max_rounds < 1, iters < 0, a resource
+ * index outside [0, R), a GPU count outside 1..ESP_MAX_GPUS, negative
+ * capacities or kappa, u_target <= 0), ESP_ERR_NONFINITE, and the errors of
+ * esp_solve.
+ */
+esp_status esp_schedule(esp_ctx *ctx, const esp_iac_model *model, int32_t max_rounds, int32_t iters, double tol,
+                        double *prices, int32_t *choice, int32_t *gpu_jobs, int32_t *rounds_used,
+                        int32_t *violations, void *stream);
+
+/*
+ * esp_read_penalties (Eq. 7): copy the context's current interference
+ * penalties Gamma (e.g. after esp_schedule) to `penalty`, host [B][nnz] in
+ * the entry order of esp_problem.  Waits for `stream`.
+ * Errors: ESP_ERR_STATE (NULL context or no penalty column),
+ * ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ */
+esp_status esp_read_penalties(esp_ctx *ctx, float *penalty, void *stream);
+
+/*
  * esp_nearest_profile (RST's profile fallback, Sec. 3.1.2 and Sec. 4.1): a
  * configuration with no profile takes the throughput of the profile-store
  * entry of its job type whose resource vector is closest in l2 distance.

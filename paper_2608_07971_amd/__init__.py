@@ -61,6 +61,17 @@ class esp_options(C.Structure):
                 ("reserved", C.c_int32 * 5)]
 
 
+class esp_iac_model(C.Structure):
+    _fields_ = [("gpus", C.c_void_p), ("gpu_memory", C.c_double), ("gpu_compute", C.c_double),
+                ("r_gpus", C.c_int32), ("r_mem", C.c_int32), ("r_sm", C.c_int32),
+                ("sensitivity", C.c_void_p), ("pressure", C.c_void_p), ("tau_base", C.c_void_p),
+                ("beta", C.c_double), ("beta_max", C.c_double), ("u_target", C.c_double), ("kappa", C.c_double)]
+
+
+ESP_MAX_GPUS = 2048
+ESP_MAX_PER_GPU = 4
+
+
 class esp_trace(C.Structure):
     _fields_ = [("prices", C.c_void_p), ("demand", C.c_void_p), ("choice", C.c_void_p)]
 
@@ -81,6 +92,9 @@ _SIGS = {
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
     "esp_loop_driver": ([C.c_void_p, C.POINTER(C.c_int32)], C.c_int),
     "esp_set_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_read_penalties": ([C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_schedule": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_void_p, C.c_void_p,
+                      C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_nearest_profile": ([C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p],
                             C.c_int),
     "esp_effective_capacity": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_double, C.c_void_p, C.c_void_p],
@@ -239,6 +253,19 @@ def esp_effective_capacity(ctx: int, queue: Optional[int], queued, gamma: float,
                                         _stream(stream)), "esp_effective_capacity")
 
 
+def esp_read_penalties(ctx: int, nnz_total: int, stream=None) -> np.ndarray:
+    out = np.empty(nnz_total, dtype=np.float32)
+    _check(lib().esp_read_penalties(ctx, out.ctypes.data, _stream(stream)), "esp_read_penalties")
+    return out
+
+
+def esp_schedule(ctx: int, model: esp_iac_model, max_rounds: int, iters: int, tol: float, prices, choice,
+                 gpu_jobs, rounds_used, violations, stream=None) -> None:
+    _check(lib().esp_schedule(ctx, C.addressof(model), int(max_rounds), int(iters), float(tol), _ptr(prices),
+                              _ptr(choice), _ptr(gpu_jobs), _ptr(rounds_used), _ptr(violations), _stream(stream)),
+           "esp_schedule")
+
+
 def esp_nearest_profile(store: int, num_queries: int, family, query, nearest, estimate=None, stream=None) -> None:
     _check(lib().esp_nearest_profile(store, int(num_queries), _ptr(family), _ptr(query), _ptr(nearest),
                                      _ptr(estimate), _stream(stream)), "esp_nearest_profile")
@@ -264,6 +291,7 @@ class Solver:
         self.device = torch.device(device)
         self.problem = Problem.from_instance(inst)
         self.B, self.N, self.R = self.problem.B, self.problem.N, self.problem.R
+        self.nnz = int(self.problem.utility.shape[1])
         self.options = esp_options(int(blocks_per_cluster), int(sweep_order), int(mode))
         nbytes = esp_workspace_size(self.problem, self.options)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
@@ -326,6 +354,39 @@ class Solver:
 
     def device_status(self, stream=None) -> int:
         return esp_device_status(self.ctx, stream)
+
+    def read_penalties(self, stream=None) -> np.ndarray:
+        """Current interference penalties Gamma, [B, nnz] float32 (host)."""
+        return esp_read_penalties(self.ctx, self.B * self.nnz, stream).reshape(self.B, self.nnz)
+
+    def schedule(self, model, prices, max_rounds: int, iters: int, tol: float = 0.0, stream=None) -> dict:
+        """Alg. 1 rounds in place on `prices`.  `model` has the fields of
+        esp_iac_model (gpus host int array [B]; sensitivity, pressure
+        float32 [B, nnz] and tau_base float64 [B, N], host or device)."""
+        dev = self.device
+
+        def on_dev(x, dt):
+            t = torch.as_tensor(np.asarray(x) if not isinstance(x, torch.Tensor) else x).to(dev, dt)
+            return t.contiguous()
+
+        gpus = np.ascontiguousarray(model.gpus, dtype=np.int32).reshape(self.B)
+        keep = {"sa": on_dev(model.sensitivity, torch.float32), "pr": on_dev(model.pressure, torch.float32),
+                "tb": on_dev(model.tau_base, torch.float64)}
+        m = esp_iac_model(gpus.ctypes.data, float(model.gpu_memory), float(model.gpu_compute), int(model.r_gpus),
+                          int(model.r_mem), int(model.r_sm), _ptr(keep["sa"]), _ptr(keep["pr"]), _ptr(keep["tb"]),
+                          float(model.beta), float(model.beta_max), float(model.u_target), float(model.kappa))
+        gmax = int(gpus.max())
+        out = {
+            "choice": torch.empty((self.B, self.N), dtype=torch.int32, device=dev),
+            "gpu_jobs": torch.empty((self.B, gmax, ESP_MAX_PER_GPU), dtype=torch.int32, device=dev),
+            "rounds": torch.empty(self.B, dtype=torch.int32, device=dev),
+            "violations": torch.empty(self.B, dtype=torch.int32, device=dev),
+        }
+        esp_schedule(self.ctx, m, max_rounds, iters, tol, prices, out["choice"], out["gpu_jobs"], out["rounds"],
+                     out["violations"], stream)
+        out["lam"] = prices
+        out["_keep"] = keep
+        return out
 
     def nearest_profile(self, family, query, stream=None):
         """RST fallback with this context as the profile store: family

@@ -21,6 +21,7 @@ using namespace esp;
 namespace {
 
 constexpr uint32_t kMagic = 0x45535031u;   // "ESP1"
+static_assert(ESP_MAX_GPUS == kMaxGpus && ESP_MAX_PER_GPU == kMaxPerGpu, "public limits match the kernels");
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -38,7 +39,7 @@ struct Plan {
     int nblk = 0;       // workgroups per cluster
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, total = 0;
+           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -151,6 +152,9 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_swc = o;   o = align_up(o + B * sizeof(double));
     pl->o_status = o; o = align_up(o + sizeof(int32_t));
     pl->o_capp = o;  o = align_up(o + B * R * sizeof(double));
+    pl->o_offs = o;  o = align_up(o + (static_cast<size_t>(pl->N) + 1) * sizeof(int64_t));
+    pl->o_inc = o;   o = align_up(o + B * static_cast<size_t>(pl->N) * sizeof(uint64_t));
+    pl->o_gpus = o;  o = align_up(o + B * sizeof(int32_t));
     pl->total = o;
     return ESP_OK;
 }
@@ -499,7 +503,10 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemsetAsync(ws + pl.o_epoch, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_swc, swc.data(), sizeof(double) * B, hipMemcpyHostToDevice, s) ==
                       hipSuccess &&
-                  hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess;
+                  hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess &&
+                  hipMemcpyAsync(ws + pl.o_offs, off.data(), sizeof(int64_t) * off.size(), hipMemcpyHostToDevice,
+                                 s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_inc, 0, sizeof(uint64_t) * static_cast<size_t>(B) * N, s) == hipSuccess;
         if (ok && pl.csr)
             ok = hipMemcpyAsync(ws + pl.o_meta, meta.data(), sizeof(TileMeta) * meta.size(), hipMemcpyHostToDevice,
                                 s) == hipSuccess &&
@@ -603,7 +610,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         KArgs a = c->base;
         a.lam_in = prices;
         a.lam_out = prices;
-        a.skip_mask = kFlagError | kFlagStopped;
+        a.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
         a.iters_done = d_iters;
         a.tol = tol;
         a.reduce = 1;
@@ -643,7 +650,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         a.lam_in = prices;
         a.choice = choice;
         a.demand_out = demand;
-        a.skip_mask = kFlagError;
+        a.skip_mask = kFlagError | kFlagFrozen;
         a.reduce = demand ? 1 : 0;
         a.reverse = (c->sweep == 0) ? static_cast<int32_t>(iters & 1) : 0;
         if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
@@ -763,6 +770,109 @@ esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_
     na.total = static_cast<int64_t>(store->pl.B) * num_queries;
     na.Q = num_queries;
     return dev(launch_nearest(store->pl.R, store->base, na, static_cast<hipStream_t>(stream)));
+}
+
+esp_status esp_schedule(esp_ctx *c, const esp_iac_model *m, int32_t max_rounds, int32_t iters, double tol,
+                        double *prices, int32_t *choice, int32_t *gpu_jobs, int32_t *rounds_used, int32_t *violations,
+                        void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (!c->pl.pen) return ESP_ERR_STATE;                 // needs the penalty column
+    if (m == nullptr || m->gpus == nullptr || m->sensitivity == nullptr || m->pressure == nullptr ||
+        m->tau_base == nullptr || prices == nullptr || choice == nullptr || gpu_jobs == nullptr ||
+        rounds_used == nullptr || violations == nullptr)
+        return ESP_ERR_INVALID_ARG;
+    const int B = c->pl.B, R = c->pl.R;
+    if (max_rounds < 1 || iters < 0) return ESP_ERR_INVALID_ARG;
+    if (m->r_gpus < 0 || m->r_gpus >= R || m->r_mem < 0 || m->r_mem >= R || m->r_sm < 0 || m->r_sm >= R)
+        return ESP_ERR_INVALID_ARG;
+    const double vals[] = {m->gpu_memory, m->gpu_compute, m->beta, m->beta_max, m->u_target, m->kappa};
+    for (double v : vals)
+        if (!std::isfinite(v)) return ESP_ERR_NONFINITE;
+    if (m->gpu_memory < 0.0 || m->gpu_compute < 0.0 || !(m->u_target > 0.0) || m->kappa < 0.0)
+        return ESP_ERR_INVALID_ARG;
+    int gmax = 0;
+    for (int b = 0; b < B; ++b) {
+        if (m->gpus[b] < 1 || m->gpus[b] > ESP_MAX_GPUS) return ESP_ERR_INVALID_ARG;
+        gmax = std::max(gmax, m->gpus[b]);
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // The pinned step-size buffer stages the GPU counts and reads back the
+    // violation counts between rounds (nothing else uses it meanwhile).
+    if (c->eta_pending) {
+        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
+        c->eta_pending = false;
+    }
+    int32_t *h32 = reinterpret_cast<int32_t *>(c->h_eta);
+    std::memcpy(h32, m->gpus, sizeof(int32_t) * B);
+    int32_t *d_gpus = reinterpret_cast<int32_t *>(c->ws + c->pl.o_gpus);
+    if (hipMemcpyAsync(d_gpus, h32, sizeof(int32_t) * B, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return ESP_ERR_DEVICE;
+    IacArgs ia;
+    ia.choice = choice;
+    ia.offsets = reinterpret_cast<const int64_t *>(c->ws + c->pl.o_offs);
+    ia.nnz = c->pl.nnz;
+    ia.gpus = d_gpus;
+    ia.gpu_memory = m->gpu_memory;
+    ia.gpu_compute = m->gpu_compute;
+    ia.r_gpus = m->r_gpus;
+    ia.r_mem = m->r_mem;
+    ia.r_sm = m->r_sm;
+    ia.sensitivity = m->sensitivity;
+    ia.pressure = m->pressure;
+    ia.tau_base = m->tau_base;
+    ia.beta = m->beta;
+    ia.beta_max = m->beta_max;
+    ia.u_target = m->u_target;
+    ia.kappa = m->kappa;
+    ia.inc = reinterpret_cast<uint64_t *>(c->ws + c->pl.o_inc);
+    ia.gpu_jobs = gpu_jobs;
+    ia.gmax = gmax;
+    ia.rounds_used = rounds_used;
+    ia.violations = violations;
+    // Alg. 1: Gamma <- 0, no cluster frozen
+    if ((st = dev(launch_iac_reset(R, c->base, B, 1, s))) != ESP_OK) return st;
+    for (int32_t r = 1; r <= max_rounds; ++r) {
+        if ((st = esp_solve(c, prices, iters, 1, tol, choice, nullptr, nullptr, nullptr, stream)) != ESP_OK) break;
+        ia.round = r;
+        if ((st = dev(launch_pack_iac(R, c->base, ia, B, s))) != ESP_OK) break;
+        if (r == max_rounds) break;
+        // stop early once every cluster is free of violations
+        if (hipMemcpyAsync(h32, violations, sizeof(int32_t) * B, hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess) {
+            st = ESP_ERR_DEVICE;
+            break;
+        }
+        bool any = false;
+        for (int b = 0; b < B; ++b) any = any || h32[b] != 0;
+        if (!any) break;
+    }
+    const esp_status st2 = dev(launch_iac_reset(R, c->base, B, 0, s));
+    return st != ESP_OK ? st : st2;
+}
+
+esp_status esp_read_penalties(esp_ctx *c, float *penalty, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (!c->pl.pen) return ESP_ERR_STATE;
+    if (penalty == nullptr) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t col_len = c->pl.col_len, ncol = c->pl.columns();
+    std::vector<float> h(col_len);
+    const int B = c->pl.B, N = c->pl.N;
+    const int64_t nnz = c->pl.nnz;
+    for (int b = 0; b < B; ++b) {
+        const float *d = reinterpret_cast<const float *>(c->ws + c->pl.o_table) +
+                         (static_cast<size_t>(b) * ncol + c->pl.R + 1) * col_len;
+        if (hipMemcpyAsync(h.data(), d, sizeof(float) * col_len, hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return ESP_ERR_DEVICE;
+        for (int j = 0; j < N; ++j)
+            for (int64_t i = 0; i < c->off[j + 1] - c->off[j]; ++i)
+                penalty[static_cast<size_t>(b) * nnz + c->off[j] + i] = std::fabs(h[c->slot_of[j] + i]);
+    }
+    return ESP_OK;
 }
 
 esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {

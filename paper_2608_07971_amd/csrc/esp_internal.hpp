@@ -21,6 +21,7 @@ constexpr int kEtaChunk = 1024;                     // iterations of step sizes 
 // Flags per cluster (device int32).
 constexpr int kFlagStopped = 1;                     // converged under tol: skip further updates
 constexpr int kFlagError = 2;                       // invalid prices: skip everything
+constexpr int kFlagFrozen = 8;                      // outer rounds: the cluster's schedule is final
 
 // Device status codes (mirror esp_status values).
 constexpr int kStatusNonfinite = 3;
@@ -120,6 +121,38 @@ struct NearestArgs {
     int64_t total;                 // B * Q
     int32_t Q;                     // queries per cluster
 };
+
+// Outer ESP-IAC rounds (Alg. 1): one wavefront per cluster packs the
+// selection onto GPUs (first fit), evaluates co-located pairs and raises the
+// penalties of offending configurations.
+constexpr int kMaxGpus = 2048;                      // GPUs per cluster (LDS-resident residuals)
+constexpr int kMaxPerGpu = 4;                       // jobs sharing one GPU
+constexpr int kMaxShards = 8;                       // GPUs of one job
+
+struct IacArgs {
+    const int32_t *choice;         // [B][N] selection of this round
+    const int64_t *offsets;        // [N+1] entry offsets of the caller's [B][nnz] arrays
+    int64_t nnz;
+    const int32_t *gpus;           // [B] GPUs per cluster
+    double gpu_memory;             // per-GPU capacity of resource r_mem
+    double gpu_compute;            // per-GPU capacity of resource r_sm
+    int32_t r_gpus, r_mem, r_sm;
+    const float *sensitivity;      // [B][nnz]
+    const float *pressure;         // [B][nnz]
+    const double *tau_base;        // [B][N]
+    double beta, beta_max, u_target, kappa;
+    uint64_t *inc;                 // [B][N] scratch, zero between rounds (bits of doubles >= 0)
+    int32_t *gpu_jobs;             // [B][gmax][kMaxPerGpu] out
+    int32_t gmax;
+    int32_t *rounds_used;          // [B] out
+    int32_t *violations;           // [B] out
+    int32_t round;                 // 1-based
+};
+
+hipError_t launch_pack_iac(int R, const KArgs &a, const IacArgs &m, int B, hipStream_t s);
+// Gamma <- 0 (interference penalties; the switching-cost marks stay) when
+// zero_gamma, and clear the frozen flags.
+hipError_t launch_iac_reset(int R, const KArgs &a, int B, int zero_gamma, hipStream_t s);
 
 hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStream_t s);
 hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s);

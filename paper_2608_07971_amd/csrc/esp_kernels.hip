@@ -18,6 +18,8 @@
 // multiple of 2^shift (the column's lowest set bit, fixed by the packer),
 // integers are added in any order, and the total is rounded once to binary64
 // (round-to-nearest-even).  No floating-point atomics are used.
+#include <algorithm>
+
 #include "esp_internal.hpp"
 
 #pragma clang fp contract(off)
@@ -1012,6 +1014,152 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
 }
 
 // ---------------------------------------------------------------------------
+// Outer ESP-IAC rounds (Sec. 3.4, Alg. 1; thresholds of Eq. 11)
+// ---------------------------------------------------------------------------
+
+// One wavefront per cluster, after the round's tatonnement and re-selection:
+//  BinPack  jobs in index order; job j at its chosen configuration needs
+//           g = d[r_gpus] GPUs (a whole number in 1..8, else not placeable)
+//           and d[r_mem] / g memory and d[r_sm] / g compute on each; it takes
+//           the g lowest-index GPUs with room for one share (all or
+//           nothing).  The lanes test 64 GPUs at a time; a ballot gives each
+//           fitting GPU its rank.  Residuals live in LDS, updated in job
+//           order by the lane owning the GPU (binary64, the oracle's order).
+//  IAC      every pair of jobs sharing a GPU: S_x|y = 1 + a_x b_y against
+//           tau_x = tau_base_x + min(beta (U / U_target - 1), beta_max),
+//           U = busy GPUs / G; a pair violates when either slowdown exceeds
+//           its threshold.  Each job keeps its largest excess (atomic max on
+//           the bit patterns of non-negative doubles).
+//  Gamma    each violating job's chosen configuration: penalty <-
+//           fp32(penalty + kappa * excess), in the packed penalty column
+//           (its sign bit, the switching-cost mark, is kept).
+// A cluster without violations is frozen: later rounds' kernels skip it.
+template <int R>
+__global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
+    __shared__ double s_mem[kMaxGpus];
+    __shared__ double s_sm[kMaxGpus];
+    __shared__ int s_cnt[kMaxGpus];
+    __shared__ int s_occ[kMaxGpus][kMaxPerGpu];
+    __shared__ int s_sel[kMaxShards];
+    const int cl = blockIdx.x;
+    const int lane = threadIdx.x;
+    if (a.flags[cl] & kFlagFrozen) return;
+    const int G = m.gpus[cl];
+    const int N = a.N;
+    float *col = const_cast<float *>(a.table) + cl * a.cluster_stride;
+    const int32_t *ch = m.choice + static_cast<size_t>(cl) * N;
+    for (int h = lane; h < G; h += kWaveSize) {
+        s_mem[h] = m.gpu_memory;
+        s_sm[h] = m.gpu_compute;
+        s_cnt[h] = 0;
+#pragma unroll
+        for (int i = 0; i < kMaxPerGpu; ++i) s_occ[h][i] = -1;
+    }
+    wave_sync();
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int j = 0; j < N; ++j) {
+        const int k = ch[j];
+        if (k < 0) continue;
+        const size_t e = (a.K > 0 ? static_cast<size_t>(j) * a.K : static_cast<size_t>(a.jobs[j].slot)) + k;
+        const double gv = static_cast<double>(col[(m.r_gpus + 1) * a.col_len + e]);
+        if (!(gv >= 1.0 && gv <= static_cast<double>(kMaxShards) && gv == floor(gv))) continue;
+        const int g = static_cast<int>(gv);
+        const double nm = static_cast<double>(col[(m.r_mem + 1) * a.col_len + e]) / gv;
+        const double ns = static_cast<double>(col[(m.r_sm + 1) * a.col_len + e]) / gv;
+        int found = 0;
+        for (int base = 0; base < G && found < g; base += kWaveSize) {
+            const int h = base + lane;
+            const bool fit = h < G && s_cnt[h] < kMaxPerGpu && s_mem[h] >= nm && s_sm[h] >= ns;
+            const uint64_t bal = __ballot(fit);
+            const int rank = found + __popcll(bal & below);
+            if (fit && rank < g) s_sel[rank] = h;
+            found += __popcll(bal);
+        }
+        wave_sync();
+        if (found >= g && lane < g) {
+            const int h = s_sel[lane];
+            s_mem[h] = s_mem[h] - nm;
+            s_sm[h] = s_sm[h] - ns;
+            s_occ[h][s_cnt[h]] = j;
+            s_cnt[h] = s_cnt[h] + 1;
+        }
+        wave_sync();
+    }
+    // thresholds of Eq. 11
+    int used = 0;
+    for (int h = lane; h < G; h += kWaveSize) used += s_cnt[h] > 0;
+#pragma unroll
+    for (int off = kWaveSize / 2; off > 0; off >>= 1) used += __shfl_xor(used, off);
+    double q = static_cast<double>(used) / static_cast<double>(G);
+    q = q / m.u_target;
+    const double w = q - 1.0;
+    double add = m.beta * w;
+    if (add > m.beta_max) add = m.beta_max;
+    const float *sa = m.sensitivity + static_cast<size_t>(cl) * m.nnz;
+    const float *pb = m.pressure + static_cast<size_t>(cl) * m.nnz;
+    const double *tb = m.tau_base + static_cast<size_t>(cl) * N;
+    unsigned long long *inc = reinterpret_cast<unsigned long long *>(m.inc) + static_cast<size_t>(cl) * N;
+    int V = 0;
+    for (int h = lane; h < G; h += kWaveSize) {
+        const int n = s_cnt[h];
+        for (int x = 0; x < n; ++x)
+            for (int y = x + 1; y < n; ++y) {
+                const int jx = s_occ[h][x], jy = s_occ[h][y];
+                const int64_t ex = m.offsets[jx] + ch[jx], ey = m.offsets[jy] + ch[jy];
+                double sxy = static_cast<double>(sa[ex]) * static_cast<double>(pb[ey]);
+                sxy = 1.0 + sxy;
+                double syx = static_cast<double>(sa[ey]) * static_cast<double>(pb[ex]);
+                syx = 1.0 + syx;
+                const double ox = sxy - (tb[jx] + add);
+                const double oy = syx - (tb[jy] + add);
+                if (ox > 0.0) atomicMax(&inc[jx], static_cast<unsigned long long>(__double_as_longlong(ox)));
+                if (oy > 0.0) atomicMax(&inc[jy], static_cast<unsigned long long>(__double_as_longlong(oy)));
+                V += (ox > 0.0 || oy > 0.0) ? 1 : 0;
+            }
+    }
+#pragma unroll
+    for (int off = kWaveSize / 2; off > 0; off >>= 1) V += __shfl_xor(V, off);
+    __threadfence();                                   // the maxima are complete before they are read
+    float *pcol = col + static_cast<size_t>(R + 1) * a.col_len;
+    for (int j = lane; j < N; j += kWaveSize) {
+        const unsigned long long bits = atomicExch(&inc[j], 0ull);
+        if (bits == 0ull) continue;
+        const double x = __longlong_as_double(static_cast<long long>(bits));
+        const size_t e = (a.K > 0 ? static_cast<size_t>(j) * a.K : static_cast<size_t>(a.jobs[j].slot)) + ch[j];
+        const uint32_t old = __float_as_uint(pcol[e]);
+        const float mag = __uint_as_float(old & 0x7fffffffu);
+        const float nv = __double2float_rn(static_cast<double>(mag) + m.kappa * x);
+        pcol[e] = __uint_as_float(__float_as_uint(nv) | (old & 0x80000000u));
+    }
+    int32_t *gj = m.gpu_jobs + static_cast<size_t>(cl) * m.gmax * kMaxPerGpu;
+    for (int h = lane; h < m.gmax; h += kWaveSize)
+#pragma unroll
+        for (int i = 0; i < kMaxPerGpu; ++i) gj[h * kMaxPerGpu + i] = h < G ? s_occ[h][i] : -1;
+    if (lane == 0) {
+        m.violations[cl] = V;
+        m.rounds_used[cl] = m.round;
+        if (V == 0) a.flags[cl] = a.flags[cl] | kFlagFrozen;
+    }
+}
+
+// Gamma <- 0 over the packed penalty columns (sign bits kept) and/or clear
+// the frozen flags.
+__global__ void k_iac_reset(float *table, size_t cluster_stride, size_t col_len, int R, int B, int32_t *flags,
+                            int zero_gamma) {
+    const size_t tid = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    if (zero_gamma) {
+        const size_t total = static_cast<size_t>(B) * col_len;
+        for (size_t i = tid; i < total; i += stride) {
+            const size_t b = i / col_len, e = i - b * col_len;
+            float *p = table + b * cluster_stride + static_cast<size_t>(R + 1) * col_len + e;
+            *p = __uint_as_float(__float_as_uint(*p) & 0x80000000u);
+        }
+    }
+    for (size_t b = tid; b < static_cast<size_t>(B); b += stride) flags[b] = flags[b] & ~kFlagFrozen;
+}
+
+// ---------------------------------------------------------------------------
 // Granular price update (esp_update_prices) and price validation
 // ---------------------------------------------------------------------------
 
@@ -1048,7 +1196,7 @@ __global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done
     if (cl >= B) return;
     bool ok = true;
     for (int r = 0; r < R; ++r) ok = ok && price_ok(lam[cl * R + r]);
-    flags[cl] = ok ? 0 : kFlagError;
+    flags[cl] = (flags[cl] & kFlagFrozen) | (ok ? 0 : kFlagError);
     if (iters_done) iters_done[cl] = 0;
     if (epoch) epoch[cl] = 0u;
     if (!ok) atomicCAS(status, 0, kStatusNonfinite);
@@ -1153,6 +1301,26 @@ hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStrea
 #define CALL(RR) launch_nearest_r<RR>(a, na, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
+}
+
+template <int R>
+static hipError_t launch_pack_iac_r(const KArgs &a, const IacArgs &m, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_pack_iac<R>), dim3(static_cast<unsigned>(B)), dim3(kWaveSize), 0, s, a, m);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_iac(int R, const KArgs &a, const IacArgs &m, int B, hipStream_t s) {
+#define CALL(RR) launch_pack_iac_r<RR>(a, m, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+hipError_t launch_iac_reset(int R, const KArgs &a, int B, int zero_gamma, hipStream_t s) {
+    const size_t work = zero_gamma ? static_cast<size_t>(B) * a.col_len : static_cast<size_t>(B);
+    const size_t blocks = std::min<size_t>((work + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_iac_reset, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                       const_cast<float *>(a.table), a.cluster_stride, a.col_len, R, B, a.flags, zero_gamma);
+    return hipGetLastError();
 }
 
 template <int R>

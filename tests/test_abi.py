@@ -146,6 +146,8 @@ def test_null_context_is_rejected():
     assert L.esp_set_capacity(None, cap, None) == esp.ESP_ERR_STATE
     assert L.esp_effective_capacity(None, None, None, 0.5, None, None) == esp.ESP_ERR_STATE
     assert L.esp_nearest_profile(None, 1, None, None, None, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_read_penalties(None, None, None) == esp.ESP_ERR_STATE
+    assert L.esp_schedule(None, None, 1, 1, 0.0, None, None, None, None, None, None) == esp.ESP_ERR_STATE
     assert L.esp_destroy(None) == esp.ESP_ERR_STATE
 
 
