@@ -1022,9 +1022,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
 //           g = d[r_gpus] GPUs (a whole number in 1..8, else not placeable)
 //           and d[r_mem] / g memory and d[r_sm] / g compute on each; it takes
 //           the g lowest-index GPUs with room for one share (all or
-//           nothing).  The lanes test 64 GPUs at a time; a ballot gives each
-//           fitting GPU its rank.  Residuals live in LDS, updated in job
-//           order by the lane owning the GPU (binary64, the oracle's order).
+//           nothing).  Jobs are gathered 64 at a time (one per lane) and
+//           placed in order; each lane tests 4 consecutive GPUs, so one step
+//           covers 256, only in blocks whose summary (largest residuals,
+//           fewest jobs) admits the share, and ballots rank the fitting
+//           GPUs.  Residuals live in LDS, updated in job order (binary64,
+//           the oracle's operations).
 //  IAC      every pair of jobs sharing a GPU: S_x|y = 1 + a_x b_y against
 //           tau_x = tau_base_x + min(beta (U / U_target - 1), beta_max),
 //           U = busy GPUs / G; a pair violates when either slowdown exceeds
@@ -1034,56 +1037,168 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
 //           fp32(penalty + kappa * excess), in the packed penalty column
 //           (its sign bit, the switching-cost mark, is kept).
 // A cluster without violations is frozen: later rounds' kernels skip it.
+// Wave-uniform copies of lane t's value (t uniform).
+__device__ __forceinline__ int lane_i(int v, int t) { return __builtin_amdgcn_readlane(v, t); }
+__device__ __forceinline__ double lane_d(double v, int t) {
+    const long long b = __double_as_longlong(v);
+    const unsigned lo = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<unsigned>(b)), t));
+    const unsigned hi = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(b >> 32), t));
+    return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+
+// Maximum of x and minimum of c over the 64 lanes (all active): DPP inside
+// each 16-lane row, then the four row results.
+__device__ __forceinline__ void wave_max2_min(double &x, double &y, int &c) {
+    x = fmax(x, dpp_d<kDppXor1>(x));
+    y = fmax(y, dpp_d<kDppXor1>(y));
+    c = min(c, dpp_i<kDppXor1>(c));
+    x = fmax(x, dpp_d<kDppXor2>(x));
+    y = fmax(y, dpp_d<kDppXor2>(y));
+    c = min(c, dpp_i<kDppXor2>(c));
+    x = fmax(x, dpp_d<kDppHalfMirror>(x));
+    y = fmax(y, dpp_d<kDppHalfMirror>(y));
+    c = min(c, dpp_i<kDppHalfMirror>(c));
+    x = fmax(x, dpp_d<kDppMirror>(x));
+    y = fmax(y, dpp_d<kDppMirror>(y));
+    c = min(c, dpp_i<kDppMirror>(c));
+    x = fmax(fmax(lane_d(x, 0), lane_d(x, 16)), fmax(lane_d(x, 32), lane_d(x, 48)));
+    y = fmax(fmax(lane_d(y, 0), lane_d(y, 16)), fmax(lane_d(y, 32), lane_d(y, 48)));
+    c = min(min(lane_i(c, 0), lane_i(c, 16)), min(lane_i(c, 32), lane_i(c, 48)));
+}
+
 template <int R>
 __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
+    constexpr int kPerLane = 4;                          // GPUs per lane in one scan step
+    constexpr int kStep = kWaveSize * kPerLane;          // GPUs per scan step
+    constexpr int kBlocks = kMaxGpus / kStep;
     __shared__ double s_mem[kMaxGpus];
     __shared__ double s_sm[kMaxGpus];
     __shared__ int s_cnt[kMaxGpus];
     __shared__ int s_occ[kMaxGpus][kMaxPerGpu];
     __shared__ int s_sel[kMaxShards];
+    static_assert(kBlocks <= kWaveSize, "one lane per block summary");
     const int cl = blockIdx.x;
     const int lane = threadIdx.x;
     if (a.flags[cl] & kFlagFrozen) return;
     const int G = m.gpus[cl];
+    const int nblk = (G + kStep - 1) / kStep;
     const int N = a.N;
     float *col = const_cast<float *>(a.table) + cl * a.cluster_stride;
     const int32_t *ch = m.choice + static_cast<size_t>(cl) * N;
-    for (int h = lane; h < G; h += kWaveSize) {
+    // GPUs beyond G get no room at all (count kMaxPerGpu), so they never fit
+    for (int h = lane; h < nblk * kStep; h += kWaveSize) {
         s_mem[h] = m.gpu_memory;
         s_sm[h] = m.gpu_compute;
-        s_cnt[h] = 0;
+        s_cnt[h] = h < G ? 0 : kMaxPerGpu;
 #pragma unroll
         for (int i = 0; i < kMaxPerGpu; ++i) s_occ[h][i] = -1;
     }
+    // Lane c < nblk keeps block c's summary in registers: largest residual
+    // memory and compute over its GPUs that can still take a job, fewest
+    // jobs.  A block failing any of the three cannot hold the share, so
+    // skipping it is exact.
+    double sum_m = m.gpu_memory, sum_s = m.gpu_compute;
+    int sum_c = lane < nblk ? 0 : kMaxPerGpu;
     wave_sync();
     const uint64_t below = (1ull << lane) - 1ull;
-    for (int j = 0; j < N; ++j) {
-        const int k = ch[j];
-        if (k < 0) continue;
-        const size_t e = (a.K > 0 ? static_cast<size_t>(j) * a.K : static_cast<size_t>(a.jobs[j].slot)) + k;
-        const double gv = static_cast<double>(col[(m.r_gpus + 1) * a.col_len + e]);
-        if (!(gv >= 1.0 && gv <= static_cast<double>(kMaxShards) && gv == floor(gv))) continue;
-        const int g = static_cast<int>(gv);
-        const double nm = static_cast<double>(col[(m.r_mem + 1) * a.col_len + e]) / gv;
-        const double ns = static_cast<double>(col[(m.r_sm + 1) * a.col_len + e]) / gv;
-        int found = 0;
-        for (int base = 0; base < G && found < g; base += kWaveSize) {
-            const int h = base + lane;
-            const bool fit = h < G && s_cnt[h] < kMaxPerGpu && s_mem[h] >= nm && s_sm[h] >= ns;
-            const uint64_t bal = __ballot(fit);
-            const int rank = found + __popcll(bal & below);
-            if (fit && rank < g) s_sel[rank] = h;
-            found += __popcll(bal);
+    // Jobs 64 at a time: each lane gathers one job's share (GPU count,
+    // memory and compute per GPU), then the wavefront places them in order.
+    for (int j0 = 0; j0 < N; j0 += kWaveSize) {
+        int g_l = 0;
+        double nm_l = 0.0, ns_l = 0.0;
+        const int jl = j0 + lane;
+        if (jl < N) {
+            const int k = ch[jl];
+            if (k >= 0) {
+                const size_t e =
+                    (a.K > 0 ? static_cast<size_t>(jl) * a.K : static_cast<size_t>(a.jobs[jl].slot)) + k;
+                const double gv = static_cast<double>(col[(m.r_gpus + 1) * a.col_len + e]);
+                if (gv >= 1.0 && gv <= static_cast<double>(kMaxShards) && gv == floor(gv)) {
+                    g_l = static_cast<int>(gv);
+                    nm_l = static_cast<double>(col[(m.r_mem + 1) * a.col_len + e]) / gv;
+                    ns_l = static_cast<double>(col[(m.r_sm + 1) * a.col_len + e]) / gv;
+                }
+            }
         }
-        wave_sync();
-        if (found >= g && lane < g) {
-            const int h = s_sel[lane];
-            s_mem[h] = s_mem[h] - nm;
-            s_sm[h] = s_sm[h] - ns;
-            s_occ[h][s_cnt[h]] = j;
-            s_cnt[h] = s_cnt[h] + 1;
+        const int cnt = min(kWaveSize, N - j0);
+        for (int t = 0; t < cnt; ++t) {
+            const int g = lane_i(g_l, t);
+            if (g == 0) continue;                          // not placeable
+            const double nm = lane_d(nm_l, t);
+            const double ns = lane_d(ns_l, t);
+            uint64_t cand = __ballot((sum_c < kMaxPerGpu) & (sum_m >= nm) & (sum_s >= ns));
+            int found = 0;
+            while (cand != 0ull && found < g) {
+                const int c = __builtin_ctzll(cand);
+                cand &= cand - 1ull;
+                // lane l tests GPUs c*256 + 4l .. 4l+3 (ascending with the lane)
+                const int h0 = c * kStep + lane * kPerLane;
+                bool fit[kPerLane];
+                uint64_t bal[kPerLane];
+                int before = 0, total = 0;
+                int cv[kPerLane];
+                double mv[kPerLane], sv[kPerLane];
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    cv[i] = s_cnt[h0 + i];
+                    mv[i] = s_mem[h0 + i];
+                    sv[i] = s_sm[h0 + i];
+                }
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    fit[i] = (cv[i] < kMaxPerGpu) & (mv[i] >= nm) & (sv[i] >= ns);
+                    bal[i] = __ballot(fit[i]);
+                    before += __popcll(bal[i] & below);
+                    total += __popcll(bal[i]);
+                }
+                int rank = found + before;
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    if (fit[i]) {
+                        if (rank < g) s_sel[rank] = h0 + i;
+                        ++rank;
+                    }
+                }
+                found += total;
+            }
+            wave_sync();
+            if (found < g) continue;                       // all or nothing
+            if (lane < g) {
+                const int h = s_sel[lane];
+                const double mh = s_mem[h], sh_ = s_sm[h];
+                const int ch_ = s_cnt[h];
+                s_mem[h] = mh - nm;
+                s_sm[h] = sh_ - ns;
+                s_occ[h][ch_] = j0 + t;
+                s_cnt[h] = ch_ + 1;
+            }
+            wave_sync();
+            // refresh the summaries of the blocks that changed
+            int last = -1;
+            for (int i = 0; i < g; ++i) {
+                const int c = s_sel[i] / kStep;
+                if (c == last) continue;
+                last = c;
+                const int h0 = c * kStep + lane * kPerLane;
+                double xm = -__builtin_inf(), xs = -__builtin_inf();
+                int xc = kMaxPerGpu;
+#pragma unroll
+                for (int q = 0; q < kPerLane; ++q) {
+                    const int cq = s_cnt[h0 + q];
+                    const double mq = s_mem[h0 + q], sq = s_sm[h0 + q];
+                    const bool open = cq < kMaxPerGpu;           // GPUs that can still take a job
+                    xm = open ? fmax(xm, mq) : xm;
+                    xs = open ? fmax(xs, sq) : xs;
+                    xc = min(xc, cq);
+                }
+                wave_max2_min(xm, xs, xc);
+                if (lane == c) {
+                    sum_m = xm;
+                    sum_s = xs;
+                    sum_c = xc;
+                }
+            }
         }
-        wave_sync();
     }
     // thresholds of Eq. 11
     int used = 0;
@@ -1122,8 +1237,9 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
     __threadfence();                                   // the maxima are complete before they are read
     float *pcol = col + static_cast<size_t>(R + 1) * a.col_len;
     for (int j = lane; j < N; j += kWaveSize) {
-        const unsigned long long bits = atomicExch(&inc[j], 0ull);
+        const unsigned long long bits = __hip_atomic_load(&inc[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (bits == 0ull) continue;
+        __hip_atomic_store(&inc[j], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const double x = __longlong_as_double(static_cast<long long>(bits));
         const size_t e = (a.K > 0 ? static_cast<size_t>(j) * a.K : static_cast<size_t>(a.jobs[j].slot)) + ch[j];
         const uint32_t old = __float_as_uint(pcol[e]);
