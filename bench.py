@@ -216,8 +216,8 @@ def _epochs(args, esp, workloads, np, torch) -> int:
     E, TOL, GAMMA, TMAX = args.epochs, 1e-3, 0.5, 1000
     act, que = workloads.epoch_market(args.epoch_jobs)
     pend = torch.from_numpy(workloads.epoch_pending(que.N, E)).cuda().contiguous()
-    a = esp.Solver(act)
-    q = esp.Solver(que)
+    a = esp.Solver(act, mode=args.mode)
+    q = esp.Solver(que, mode=args.mode)
     stream = torch.cuda.Stream()
     print(f"[bench] epochs: active N={act.N} nnz={act.nnz} queue N={que.N} nnz={que.nnz} R={act.R} E={E}",
           file=sys.stderr, flush=True)
@@ -285,7 +285,7 @@ def _nearest(args, esp, workloads, np, torch) -> int:
     fam_np, q_np = workloads.nn_queries(store, args.nearest, seed=9)
     fam = torch.from_numpy(fam_np).cuda()
     q = torch.from_numpy(q_np).cuda()
-    s = esp.Solver(store)
+    s = esp.Solver(store, mode=args.mode)
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         for _ in range(max(1, args.warmup)):
@@ -335,7 +335,7 @@ def _schedule(args, esp, workloads, np, torch) -> int:
     model.pressure = torch.from_numpy(model.pressure).cuda()
     model.tau_base = torch.from_numpy(model.tau_base).cuda()
     T = args.iters or 5
-    s = esp.Solver(inst)
+    s = esp.Solver(inst, mode=args.mode)
     lam0 = s.prices(inst.lam0)
     lam = lam0.clone()
     stream = torch.cuda.Stream()
