@@ -390,7 +390,7 @@ def _schedule(args, esp, workloads, np, torch) -> int:
 def _kernel_sha() -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in ("esp_kernels.hip", "esp_internal.hpp"):
+    for f in ("esp_kernels.hip", "esp_device.hpp", "esp_internal.hpp"):
         h.update(open(os.path.join(ROOT, "paper_2608_07971_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 

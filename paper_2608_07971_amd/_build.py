@@ -8,7 +8,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libesp.so")
-SOURCES = ["esp_api.hip", "esp_kernels.hip"]
+SOURCES = ["esp_api.hip", "esp_kernels.hip", "esp_extras.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "../../include/esp.h"
+#include "esp_extras.hpp"
 #include "esp_internal.hpp"
 
 #pragma clang fp contract(off)

@@ -1,0 +1,213 @@
+// Device helpers shared by the gfx950 kernels of the Elastic Shadow Pricing
+// library: DPP lane moves and the lowest-index argmax, exact fixed-point
+// sums, and the cross-workgroup completion of a cluster's sums.
+#pragma once
+
+#include "esp_internal.hpp"
+
+#pragma clang fp contract(off)
+
+namespace esp {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned __int128 u128;
+
+// ---------------------------------------------------------------------------
+// Wavefront primitives
+// ---------------------------------------------------------------------------
+
+// DPP lane moves inside 16-lane rows.
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // lane i <- lane 7-i within each 8 lanes
+constexpr int kDppMirror = 0x140;       // lane i <- lane 15-i within each row
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = dpp_i<CTRL>(static_cast<int>(static_cast<unsigned>(b)));
+    const int hi = dpp_i<CTRL>(static_cast<int>(b >> 32));
+    return __longlong_as_double(static_cast<long long>(
+        (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+
+// (os, ok) replaces (s, k) when its score is larger, or equal with a lower
+// configuration index.  This is a total order on (score, -index) for the
+// non-NaN scores the kernels produce, so any reduction tree returns the
+// entry a sequential lowest-index scan would.
+__device__ __forceinline__ void take_better(double &s, int &k, double os, int ok) {
+    const bool b = (os > s) || (os == s && ok < k);
+    s = b ? os : s;
+    k = b ? ok : k;
+}
+
+// The penalty of the ESP score (Eq. 7) after the rent: the switching cost when
+// the stored penalty's sign bit marks "not the current configuration", then
+// the interference penalty |p|.
+__device__ __forceinline__ double penalize(double sc, float p, double sw) {
+    if (__float_as_uint(p) >> 31) sc = sc - sw;
+    return sc - static_cast<double>(fabsf(p));
+}
+
+// Argmax over aligned groups of LPJ lanes (LPJ in {1,2,4,8,16}); afterwards
+// every lane of a group holds the group's winner.
+template <int LPJ>
+__device__ __forceinline__ void group_argmax(double &s, int &k) {
+    if constexpr (LPJ >= 2) take_better(s, k, dpp_d<kDppXor1>(s), dpp_i<kDppXor1>(k));
+    if constexpr (LPJ >= 4) take_better(s, k, dpp_d<kDppXor2>(s), dpp_i<kDppXor2>(k));
+    if constexpr (LPJ >= 8) take_better(s, k, dpp_d<kDppHalfMirror>(s), dpp_i<kDppHalfMirror>(k));
+    if constexpr (LPJ >= 16) take_better(s, k, dpp_d<kDppMirror>(s), dpp_i<kDppMirror>(k));
+}
+
+// Compiler-level ordering of LDS traffic inside one wavefront.
+__device__ __forceinline__ void wave_sync() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_wave_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// ---------------------------------------------------------------------------
+// Exact fixed-point demand accumulation
+// ---------------------------------------------------------------------------
+
+// v (finite, +0.0 or positive) as an integer multiple of 2^sh in an
+// accumulator type A (64- or 128-bit, chosen by the packer per problem).  The
+// packer guarantees that every nonzero value of the column has its lowest set
+// bit at or above 2^sh and its highest below 2^(sh + bits(A) - 1 -
+// ceil(log2(N + 1))), so the shift is exact and N of them cannot overflow A.
+template <typename A>
+__device__ __forceinline__ A fx_of(float v, int sh) {
+    constexpr int kMax = static_cast<int>(sizeof(A)) * 8 - 1;
+    const uint32_t bits = __float_as_uint(v);
+    const uint32_t e = bits >> 23;
+    const uint32_t m = (bits & 0x7fffffu) | (e ? 0x800000u : 0u);
+    int s = (e ? static_cast<int>(e) : 1) - 150 - sh;
+    if (m == 0) return 0;
+    s = s > kMax ? kMax : (s < -kMax ? -kMax : s);
+    const A mm = m;
+    return s >= 0 ? (mm << s) : (mm >> (-s));
+}
+
+// Round a * 2^sh to the nearest binary64, ties to even.
+__device__ __forceinline__ double fx_to_double(u128 a, int sh) {
+    if (a == 0) return 0.0;
+    const uint64_t hi = static_cast<uint64_t>(a >> 64);
+    const uint64_t lo = static_cast<uint64_t>(a);
+    const int h = hi ? 127 - __clzll(hi) : 63 - __clzll(lo);
+    if (h <= 52) return ldexp(static_cast<double>(lo), sh);
+    const int drop = h - 52;
+    uint64_t m = static_cast<uint64_t>(a >> drop);
+    const u128 rem = a & ((static_cast<u128>(1) << drop) - 1);
+    const u128 half = static_cast<u128>(1) << (drop - 1);
+    if (rem > half || (rem == half && (m & 1u))) m += 1;   // m <= 2^53: exact as a double
+    return ldexp(static_cast<double>(m), drop + sh);
+}
+
+// Cross-workgroup exact sums of one cluster.  bsum[r] (LDS) holds this
+// workgroup's 128-bit sum for resource r.  In the workgroup that finishes
+// last, thread r < R runs done(r, total_r) with the cluster's total; the
+// function returns true there (after a workgroup barrier) and false in every
+// other workgroup.
+//
+// Ordering across the 8 XCDs (each with its own L2) without cache-wide
+// writeback or invalidation: wavefront 0 publishes the partial with
+// agent-scope atomic exchanges, which are performed at the device coherence
+// point and have completed once their old values are back; it waits for them
+// (s_waitcnt vmcnt(0) on the returned values) before it takes a ticket with
+// an agent-scope atomic add.  The workgroup that draws the last ticket reads
+// every partial with agent-scope atomic loads, which bypass the non-coherent
+// caches, and resets the ticket for the next use.
+template <int R, typename Done>
+__device__ __forceinline__ bool cluster_sums(const KArgs &a, int cl, int blk, const u128 *bsum, Done &&done) {
+    __shared__ int s_last;
+    __shared__ u128 s_red[kBlockThreads];
+    const int t = threadIdx.x;
+    if (a.nblk == 1) {
+        // One workgroup per cluster: its own sums are the totals.
+        if (t < R) s_red[t] = bsum[t];
+        __syncthreads();
+        if (t < R) done(t, s_red[t]);
+        __syncthreads();
+        return true;
+    }
+    if (t < kWaveSize) {
+        uint64_t old = 0;
+        if (t < R) {
+            uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + blk) * R + t) * 2;
+            const u128 v = bsum[t];
+            old ^= __hip_atomic_exchange(p, static_cast<uint64_t>(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            old ^= __hip_atomic_exchange(p + 1, static_cast<uint64_t>(v >> 64), __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" : : "v"(old) : "memory");
+        if (t == 0) {
+            const unsigned prev = __hip_atomic_fetch_add(&a.tickets[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
+        }
+    }
+    __syncthreads();
+    if (!s_last) return false;
+
+    // Sum the nblk partials of each resource: thread (g, r) takes blocks
+    // g, g+G, g+2G, ...; eight independent loads in flight per thread.
+    constexpr int G = kBlockThreads / R;
+    constexpr int U = 8;
+    u128 s = 0;
+    if (t < G * R) {
+        const int r = t % R, g = t / R;
+        const uint64_t *base = a.partials + (static_cast<size_t>(cl) * a.nblk * R + r) * 2;
+#pragma unroll 1
+        for (int b0 = g; b0 < a.nblk; b0 += U * G) {
+            u128 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int b = b0 + u * G;
+                v[u] = 0;
+                if (b < a.nblk) {
+                    uint64_t *p = const_cast<uint64_t *>(base) + static_cast<size_t>(b) * R * 2;
+                    const uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    v[u] = (static_cast<u128>(hi) << 64) | lo;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) s += v[u];
+        }
+    }
+    s_red[t] = s;
+    __syncthreads();
+    if (t < R) {
+        u128 tot = 0;
+#pragma unroll 1
+        for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
+        done(t, tot);
+    }
+    if (t == 0) {
+        // ready for the next use
+        const unsigned o = __hip_atomic_exchange(&a.tickets[cl], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" : : "v"(o) : "memory");
+    }
+    __syncthreads();
+    return true;
+}
+
+}  // namespace esp
+
+// Runtime R -> template instance of a launcher.
+#define ESP_DISPATCH_R(R, CALL)              \
+    switch (R) {                             \
+        case 1: return CALL(1);              \
+        case 2: return CALL(2);              \
+        case 3: return CALL(3);              \
+        case 4: return CALL(4);              \
+        case 5: return CALL(5);              \
+        case 6: return CALL(6);              \
+        case 7: return CALL(7);              \
+        case 8: return CALL(8);              \
+        default: return hipErrorInvalidValue; \
+    }

@@ -1,0 +1,531 @@
+// gfx950 kernels beyond the price loop: the effective capacity of Eq. 12,
+// the outer ESP-IAC rounds of Alg. 1 and RST's nearest-profile fallback.
+#include <algorithm>
+
+#include "esp_device.hpp"
+#include "esp_extras.hpp"
+
+#pragma clang fp contract(off)
+
+namespace esp {
+
+// ---------------------------------------------------------------------------
+// Effective capacity (Sec. 3.4, Eq. 12)
+// ---------------------------------------------------------------------------
+
+// C_eff_r = C_r - gamma * S_r, S_r = sum over pending jobs j of
+// min over j's allowed configurations of d_jkr (the componentwise smallest
+// footprint), over the pending jobs' own packed table.  A wavefront takes one
+// tile at a time: each lane folds its 4 entries into one minimum per job
+// piece (entries of one job are adjacent) and merges it into the tile's
+// per-job minima in LDS with an unsigned atomic minimum (demands are
+// non-negative floats with +0.0 for zero, whose bit patterns order like the
+// values); the lanes then add the minima of pending jobs to exact fixed-point
+// accumulators.  Masked configurations and padding carry a utility of -inf
+// (dense padding: job index >= N) and are skipped.
+template <int R, typename A>
+__global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs ra) {
+    constexpr uint32_t kInf = 0x7f800000u;
+    __shared__ uint32_t s_min[kBlockWaves][kTileEntries][R];
+    __shared__ u128 s_part[kBlockWaves][R];
+    __shared__ u128 s_bsum[R];
+    const int cl = blockIdx.x / a.nblk;
+    const int blk = blockIdx.x - cl * a.nblk;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wave = threadIdx.x / kWaveSize;
+    const float *col = a.table + cl * a.cluster_stride;
+    const uint8_t *pend = ra.queued ? ra.queued + static_cast<size_t>(cl) * a.N : nullptr;
+    int sh[R];
+    A acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        sh[r] = a.shift[cl * R + r];
+        acc[r] = 0;
+    }
+    uint32_t *mins = &s_min[wave][0][0];
+    for (int i = lane; i < kTileEntries * R; i += kWaveSize) mins[i] = kInf;
+    wave_sync();
+    const int jpt = a.K > 0 ? kTileEntries / a.K : 0;          // dense: jobs per tile
+    for (int tile = blk * kBlockWaves + wave; tile < a.tiles; tile += a.nblk * kBlockWaves) {
+        const size_t base = static_cast<size_t>(tile) * kTileEntries + static_cast<size_t>(lane) * 4;
+        const f4 u = *reinterpret_cast<const f4 *>(col + base);
+        f4 d[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) d[r] = *reinterpret_cast<const f4 *>(col + (r + 1) * a.col_len + base);
+        int first_job, njobs, jt;
+        uint32_t heads;                        // bit i: entry 4*lane + i starts a job
+        if (a.K > 0) {
+            first_job = tile * jpt;
+            njobs = min(jpt, a.N - first_job);
+            jt = (lane * 4) / a.K;
+            heads = 0;                         // K >= 4: a lane's 4 entries share one job
+        } else {
+            const TileMeta &m = a.meta[tile];
+            const int e0 = lane * 4, w = e0 >> 5, bit = e0 & 31;
+            int before = 0, total = 0;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int c = __popc(m.head[q]);
+                total += c;
+                before += (q < w) ? c : 0;
+            }
+            const uint32_t word = m.head[w];
+            const uint32_t upto = (bit == 31) ? 0xffffffffu : ((2u << bit) - 1u);
+            first_job = static_cast<int>(m.first_job);
+            njobs = total;
+            jt = before + __popc(word & upto) - 1; // entry 0 of a tile always starts a job
+            heads = (word >> bit) & 0xfu;
+        }
+        uint32_t mn[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) mn[r] = kInf;
+        auto flush = [&]() {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (mn[r] != kInf) atomicMin(&s_min[wave][jt][r], mn[r]);
+        };
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (i > 0 && ((heads >> i) & 1u)) {
+                flush();
+                ++jt;
+#pragma unroll
+                for (int r = 0; r < R; ++r) mn[r] = kInf;
+            }
+            const bool valid = (u[i] != -__builtin_inff()) && (jt < njobs);
+            if (valid) {
+#pragma unroll
+                for (int r = 0; r < R; ++r) mn[r] = min(mn[r], __float_as_uint(d[r][i]));
+            }
+        }
+        flush();
+        wave_sync();
+        for (int q = lane; q < njobs; q += kWaveSize) {
+            const bool take = !pend || pend[first_job + q] != 0;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const uint32_t m = s_min[wave][q][r];
+                s_min[wave][q][r] = kInf;
+                if (take && m != kInf) acc[r] += fx_of<A>(__uint_as_float(m), sh[r]);
+            }
+        }
+        wave_sync();
+    }
+    // workgroup sums: wavefront tree over lanes, then the 4 wavefronts in order
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        u128 v = static_cast<u128>(acc[r]);
+#pragma unroll
+        for (int off = kWaveSize / 2; off > 0; off >>= 1) {
+            const unsigned long long lo = __shfl_down(static_cast<unsigned long long>(v), off);
+            const unsigned long long hi = __shfl_down(static_cast<unsigned long long>(v >> 64), off);
+            v += (static_cast<u128>(hi) << 64) | lo;
+        }
+        if (lane == 0) s_part[wave][r] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < R) {
+        u128 t = 0;
+        for (int w = 0; w < kBlockWaves; ++w) t += s_part[w][threadIdx.x];
+        s_bsum[threadIdx.x] = t;
+    }
+    __syncthreads();
+    cluster_sums<R>(a, cl, blk, s_bsum, [&](int r, u128 tot) {
+        const double S = fx_to_double(tot, a.shift[cl * R + r]);
+        const double g = ra.gamma * S;
+        const double ce = ra.cap_phys[cl * R + r] - g;
+        ra.cap_eff[cl * R + r] = ce;
+        if (ra.out) ra.out[cl * R + r] = ce;
+    });
+}
+
+// ---------------------------------------------------------------------------
+// Nearest-profile fallback of RST (Sec. 3.1.2, Sec. 4.1)
+// ---------------------------------------------------------------------------
+
+constexpr int kNearestLanes = 16;                     // lanes per query (one DPP row)
+
+// Query i of a cluster names a job type f and an unprofiled configuration's
+// resource vector q.  The 16 lanes of one DPP row serve one query: lane s
+// takes entries s, s+16, ... of family f, skips masked ones (utility -inf),
+// and keeps the smallest squared l2 distance, computed in binary64 in a fixed
+// order (e_0 = q_0 - d_0, acc = e_0 e_0, acc = acc + e_r e_r for r = 1..R-1).
+// The row then takes the argmax of the negated distance with lowest-index
+// ties (group_argmax), i.e. the nearest entry with the lowest index among
+// equals; lane 0 writes its index and its throughput (the utility column).
+// A family index out of range or a non-finite query component gives -1 /
+// NaN and records an error.
+template <int R>
+__global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs na) {
+    constexpr int kPerBlock = kBlockThreads / kNearestLanes;
+    const int sub = threadIdx.x & (kNearestLanes - 1);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kPerBlock;
+    // every lane of a row shares gi, so rows stay whole for the DPP steps
+    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kPerBlock + threadIdx.x / kNearestLanes; gi < na.total;
+         gi += stride) {
+        const int cl = static_cast<int>(gi / na.Q);
+        const float *col = a.table + cl * a.cluster_stride;
+        const int f = na.family[gi];
+        double q[R];
+        bool ok = f >= 0 && f < a.N;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const float v = na.query[gi * R + r];
+            ok = ok && (fabsf(v) <= 3.402823466e38f);     // false for NaN and +-inf
+            q[r] = static_cast<double>(v);
+        }
+        double best = -__builtin_inf();
+        int bk = 0x7fffffff;
+        uint32_t slot = 0;
+        if (ok) {
+            uint32_t size;
+            if (a.K > 0) {
+                slot = static_cast<uint32_t>(f) * static_cast<uint32_t>(a.K);
+                size = static_cast<uint32_t>(a.K);
+            } else {
+                slot = a.jobs[f].slot;
+                size = a.jobs[f].size;
+            }
+            for (uint32_t k = sub; k < size; k += kNearestLanes) {
+                const size_t e = static_cast<size_t>(slot) + k;
+                if (col[e] == -__builtin_inff()) continue;     // masked configuration
+                double x = q[0] - static_cast<double>(col[a.col_len + e]);
+                double acc = x * x;
+#pragma unroll
+                for (int r = 1; r < R; ++r) {
+                    x = q[r] - static_cast<double>(col[(r + 1) * a.col_len + e]);
+                    acc = acc + x * x;
+                }
+                take_better(best, bk, -acc, static_cast<int>(k));
+            }
+        }
+        group_argmax<kNearestLanes>(best, bk);
+        if (sub == 0) {
+            const bool found = ok && bk != 0x7fffffff;
+            na.nearest[gi] = found ? bk : -1;
+            if (na.estimate)
+                na.estimate[gi] = found ? col[static_cast<size_t>(slot) + static_cast<uint32_t>(bk)] : __builtin_nanf("");
+            if (!ok) atomicCAS(a.status, 0, (f >= 0 && f < a.N) ? kStatusNonfinite : kStatusInvalid);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Outer ESP-IAC rounds (Sec. 3.4, Alg. 1; thresholds of Eq. 11)
+// ---------------------------------------------------------------------------
+
+// One wavefront per cluster, after the round's tatonnement and re-selection:
+//  BinPack  jobs in index order; job j at its chosen configuration needs
+//           g = d[r_gpus] GPUs (a whole number in 1..8, else not placeable)
+//           and d[r_mem] / g memory and d[r_sm] / g compute on each; it takes
+//           the g lowest-index GPUs with room for one share (all or
+//           nothing).  Jobs are gathered 64 at a time (one per lane) and
+//           placed in order; each lane tests 4 consecutive GPUs, so one step
+//           covers 256, only in blocks whose summary (largest residuals,
+//           fewest jobs) admits the share, and ballots rank the fitting
+//           GPUs.  Residuals live in LDS, updated in job order (binary64,
+//           the oracle's operations).
+//  IAC      every pair of jobs sharing a GPU: S_x|y = 1 + a_x b_y against
+//           tau_x = tau_base_x + min(beta (U / U_target - 1), beta_max),
+//           U = busy GPUs / G; a pair violates when either slowdown exceeds
+//           its threshold.  Each job keeps its largest excess (atomic max on
+//           the bit patterns of non-negative doubles).
+//  Gamma    each violating job's chosen configuration: penalty <-
+//           fp32(penalty + kappa * excess), in the packed penalty column
+//           (its sign bit, the switching-cost mark, is kept).
+// A cluster without violations is frozen: later rounds' kernels skip it.
+// Wave-uniform copies of lane t's value (t uniform).
+__device__ __forceinline__ int lane_i(int v, int t) { return __builtin_amdgcn_readlane(v, t); }
+__device__ __forceinline__ double lane_d(double v, int t) {
+    const long long b = __double_as_longlong(v);
+    const unsigned lo = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<unsigned>(b)), t));
+    const unsigned hi = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(b >> 32), t));
+    return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+
+// Maximum of x and minimum of c over the 64 lanes (all active): DPP inside
+// each 16-lane row, then the four row results.
+__device__ __forceinline__ void wave_max2_min(double &x, double &y, int &c) {
+    x = fmax(x, dpp_d<kDppXor1>(x));
+    y = fmax(y, dpp_d<kDppXor1>(y));
+    c = min(c, dpp_i<kDppXor1>(c));
+    x = fmax(x, dpp_d<kDppXor2>(x));
+    y = fmax(y, dpp_d<kDppXor2>(y));
+    c = min(c, dpp_i<kDppXor2>(c));
+    x = fmax(x, dpp_d<kDppHalfMirror>(x));
+    y = fmax(y, dpp_d<kDppHalfMirror>(y));
+    c = min(c, dpp_i<kDppHalfMirror>(c));
+    x = fmax(x, dpp_d<kDppMirror>(x));
+    y = fmax(y, dpp_d<kDppMirror>(y));
+    c = min(c, dpp_i<kDppMirror>(c));
+    x = fmax(fmax(lane_d(x, 0), lane_d(x, 16)), fmax(lane_d(x, 32), lane_d(x, 48)));
+    y = fmax(fmax(lane_d(y, 0), lane_d(y, 16)), fmax(lane_d(y, 32), lane_d(y, 48)));
+    c = min(min(lane_i(c, 0), lane_i(c, 16)), min(lane_i(c, 32), lane_i(c, 48)));
+}
+
+template <int R>
+__global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
+    constexpr int kPerLane = 4;                          // GPUs per lane in one scan step
+    constexpr int kStep = kWaveSize * kPerLane;          // GPUs per scan step
+    constexpr int kBlocks = kMaxGpus / kStep;
+    __shared__ double s_mem[kMaxGpus];
+    __shared__ double s_sm[kMaxGpus];
+    __shared__ int s_cnt[kMaxGpus];
+    __shared__ int s_occ[kMaxGpus][kMaxPerGpu];
+    __shared__ int s_sel[kMaxShards];
+    static_assert(kBlocks <= kWaveSize, "one lane per block summary");
+    const int cl = blockIdx.x;
+    const int lane = threadIdx.x;
+    if (a.flags[cl] & kFlagFrozen) return;
+    const int G = m.gpus[cl];
+    const int nblk = (G + kStep - 1) / kStep;
+    const int N = a.N;
+    float *col = const_cast<float *>(a.table) + cl * a.cluster_stride;
+    const int32_t *ch = m.choice + static_cast<size_t>(cl) * N;
+    // GPUs beyond G get no room at all (count kMaxPerGpu), so they never fit
+    for (int h = lane; h < nblk * kStep; h += kWaveSize) {
+        s_mem[h] = m.gpu_memory;
+        s_sm[h] = m.gpu_compute;
+        s_cnt[h] = h < G ? 0 : kMaxPerGpu;
+#pragma unroll
+        for (int i = 0; i < kMaxPerGpu; ++i) s_occ[h][i] = -1;
+    }
+    // Lane c < nblk keeps block c's summary in registers: largest residual
+    // memory and compute over its GPUs that can still take a job, fewest
+    // jobs.  A block failing any of the three cannot hold the share, so
+    // skipping it is exact.
+    double sum_m = m.gpu_memory, sum_s = m.gpu_compute;
+    int sum_c = lane < nblk ? 0 : kMaxPerGpu;
+    wave_sync();
+    const uint64_t below = (1ull << lane) - 1ull;
+    // Jobs 64 at a time: each lane gathers one job's share (GPU count,
+    // memory and compute per GPU), then the wavefront places them in order.
+    for (int j0 = 0; j0 < N; j0 += kWaveSize) {
+        int g_l = 0;
+        double nm_l = 0.0, ns_l = 0.0;
+        const int jl = j0 + lane;
+        if (jl < N) {
+            const int k = ch[jl];
+            if (k >= 0) {
+                const size_t e =
+                    (a.K > 0 ? static_cast<size_t>(jl) * a.K : static_cast<size_t>(a.jobs[jl].slot)) + k;
+                const double gv = static_cast<double>(col[(m.r_gpus + 1) * a.col_len + e]);
+                if (gv >= 1.0 && gv <= static_cast<double>(kMaxShards) && gv == floor(gv)) {
+                    g_l = static_cast<int>(gv);
+                    nm_l = static_cast<double>(col[(m.r_mem + 1) * a.col_len + e]) / gv;
+                    ns_l = static_cast<double>(col[(m.r_sm + 1) * a.col_len + e]) / gv;
+                }
+            }
+        }
+        const int cnt = min(kWaveSize, N - j0);
+        for (int t = 0; t < cnt; ++t) {
+            const int g = lane_i(g_l, t);
+            if (g == 0) continue;                          // not placeable
+            const double nm = lane_d(nm_l, t);
+            const double ns = lane_d(ns_l, t);
+            uint64_t cand = __ballot((sum_c < kMaxPerGpu) & (sum_m >= nm) & (sum_s >= ns));
+            int found = 0;
+            while (cand != 0ull && found < g) {
+                const int c = __builtin_ctzll(cand);
+                cand &= cand - 1ull;
+                // lane l tests GPUs c*256 + 4l .. 4l+3 (ascending with the lane)
+                const int h0 = c * kStep + lane * kPerLane;
+                bool fit[kPerLane];
+                uint64_t bal[kPerLane];
+                int before = 0, total = 0;
+                int cv[kPerLane];
+                double mv[kPerLane], sv[kPerLane];
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    cv[i] = s_cnt[h0 + i];
+                    mv[i] = s_mem[h0 + i];
+                    sv[i] = s_sm[h0 + i];
+                }
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    fit[i] = (cv[i] < kMaxPerGpu) & (mv[i] >= nm) & (sv[i] >= ns);
+                    bal[i] = __ballot(fit[i]);
+                    before += __popcll(bal[i] & below);
+                    total += __popcll(bal[i]);
+                }
+                int rank = found + before;
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    if (fit[i]) {
+                        if (rank < g) s_sel[rank] = h0 + i;
+                        ++rank;
+                    }
+                }
+                found += total;
+            }
+            wave_sync();
+            if (found < g) continue;                       // all or nothing
+            if (lane < g) {
+                const int h = s_sel[lane];
+                const double mh = s_mem[h], sh_ = s_sm[h];
+                const int ch_ = s_cnt[h];
+                s_mem[h] = mh - nm;
+                s_sm[h] = sh_ - ns;
+                s_occ[h][ch_] = j0 + t;
+                s_cnt[h] = ch_ + 1;
+            }
+            wave_sync();
+            // refresh the summaries of the blocks that changed
+            int last = -1;
+            for (int i = 0; i < g; ++i) {
+                const int c = s_sel[i] / kStep;
+                if (c == last) continue;
+                last = c;
+                const int h0 = c * kStep + lane * kPerLane;
+                double xm = -__builtin_inf(), xs = -__builtin_inf();
+                int xc = kMaxPerGpu;
+#pragma unroll
+                for (int q = 0; q < kPerLane; ++q) {
+                    const int cq = s_cnt[h0 + q];
+                    const double mq = s_mem[h0 + q], sq = s_sm[h0 + q];
+                    const bool open = cq < kMaxPerGpu;           // GPUs that can still take a job
+                    xm = open ? fmax(xm, mq) : xm;
+                    xs = open ? fmax(xs, sq) : xs;
+                    xc = min(xc, cq);
+                }
+                wave_max2_min(xm, xs, xc);
+                if (lane == c) {
+                    sum_m = xm;
+                    sum_s = xs;
+                    sum_c = xc;
+                }
+            }
+        }
+    }
+    // thresholds of Eq. 11
+    int used = 0;
+    for (int h = lane; h < G; h += kWaveSize) used += s_cnt[h] > 0;
+#pragma unroll
+    for (int off = kWaveSize / 2; off > 0; off >>= 1) used += __shfl_xor(used, off);
+    double q = static_cast<double>(used) / static_cast<double>(G);
+    q = q / m.u_target;
+    const double w = q - 1.0;
+    double add = m.beta * w;
+    if (add > m.beta_max) add = m.beta_max;
+    const float *sa = m.sensitivity + static_cast<size_t>(cl) * m.nnz;
+    const float *pb = m.pressure + static_cast<size_t>(cl) * m.nnz;
+    const double *tb = m.tau_base + static_cast<size_t>(cl) * N;
+    unsigned long long *inc = reinterpret_cast<unsigned long long *>(m.inc) + static_cast<size_t>(cl) * N;
+    int V = 0;
+    for (int h = lane; h < G; h += kWaveSize) {
+        const int n = s_cnt[h];
+        for (int x = 0; x < n; ++x)
+            for (int y = x + 1; y < n; ++y) {
+                const int jx = s_occ[h][x], jy = s_occ[h][y];
+                const int64_t ex = m.offsets[jx] + ch[jx], ey = m.offsets[jy] + ch[jy];
+                double sxy = static_cast<double>(sa[ex]) * static_cast<double>(pb[ey]);
+                sxy = 1.0 + sxy;
+                double syx = static_cast<double>(sa[ey]) * static_cast<double>(pb[ex]);
+                syx = 1.0 + syx;
+                const double ox = sxy - (tb[jx] + add);
+                const double oy = syx - (tb[jy] + add);
+                if (ox > 0.0) atomicMax(&inc[jx], static_cast<unsigned long long>(__double_as_longlong(ox)));
+                if (oy > 0.0) atomicMax(&inc[jy], static_cast<unsigned long long>(__double_as_longlong(oy)));
+                V += (ox > 0.0 || oy > 0.0) ? 1 : 0;
+            }
+    }
+#pragma unroll
+    for (int off = kWaveSize / 2; off > 0; off >>= 1) V += __shfl_xor(V, off);
+    __threadfence();                                   // the maxima are complete before they are read
+    float *pcol = col + static_cast<size_t>(R + 1) * a.col_len;
+    for (int j = lane; j < N; j += kWaveSize) {
+        const unsigned long long bits = __hip_atomic_load(&inc[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (bits == 0ull) continue;
+        __hip_atomic_store(&inc[j], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const double x = __longlong_as_double(static_cast<long long>(bits));
+        const size_t e = (a.K > 0 ? static_cast<size_t>(j) * a.K : static_cast<size_t>(a.jobs[j].slot)) + ch[j];
+        const uint32_t old = __float_as_uint(pcol[e]);
+        const float mag = __uint_as_float(old & 0x7fffffffu);
+        const float nv = __double2float_rn(static_cast<double>(mag) + m.kappa * x);
+        pcol[e] = __uint_as_float(__float_as_uint(nv) | (old & 0x80000000u));
+    }
+    int32_t *gj = m.gpu_jobs + static_cast<size_t>(cl) * m.gmax * kMaxPerGpu;
+    for (int h = lane; h < m.gmax; h += kWaveSize)
+#pragma unroll
+        for (int i = 0; i < kMaxPerGpu; ++i) gj[h * kMaxPerGpu + i] = h < G ? s_occ[h][i] : -1;
+    if (lane == 0) {
+        m.violations[cl] = V;
+        m.rounds_used[cl] = m.round;
+        if (V == 0) a.flags[cl] = a.flags[cl] | kFlagFrozen;
+    }
+}
+
+// Gamma <- 0 over the packed penalty columns (sign bits kept) and/or clear
+// the frozen flags.
+__global__ void k_iac_reset(float *table, size_t cluster_stride, size_t col_len, int R, int B, int32_t *flags,
+                            int zero_gamma) {
+    const size_t tid = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+    if (zero_gamma) {
+        const size_t total = static_cast<size_t>(B) * col_len;
+        for (size_t i = tid; i < total; i += stride) {
+            const size_t b = i / col_len, e = i - b * col_len;
+            float *p = table + b * cluster_stride + static_cast<size_t>(R + 1) * col_len + e;
+            *p = __uint_as_float(__float_as_uint(*p) & 0x80000000u);
+        }
+    }
+    for (size_t b = tid; b < static_cast<size_t>(B); b += stride) flags[b] = flags[b] & ~kFlagFrozen;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------
+
+template <int R>
+static hipError_t launch_nearest_r(const KArgs &a, const NearestArgs &na, hipStream_t s) {
+    constexpr int kPerBlock = kBlockThreads / kNearestLanes;
+    const int64_t need = (na.total + kPerBlock - 1) / kPerBlock;
+    const int64_t cap = 256 * 32;                    // enough resident queries to cover gather latency
+    const dim3 grid(static_cast<unsigned>(need < cap ? need : cap)), block(kBlockThreads);
+    hipLaunchKernelGGL((k_nearest<R>), grid, block, 0, s, a, na);
+    return hipGetLastError();
+}
+
+hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStream_t s) {
+#define CALL(RR) launch_nearest_r<RR>(a, na, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_pack_iac_r(const KArgs &a, const IacArgs &m, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_pack_iac<R>), dim3(static_cast<unsigned>(B)), dim3(kWaveSize), 0, s, a, m);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_iac(int R, const KArgs &a, const IacArgs &m, int B, hipStream_t s) {
+#define CALL(RR) launch_pack_iac_r<RR>(a, m, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+hipError_t launch_iac_reset(int R, const KArgs &a, int B, int zero_gamma, hipStream_t s) {
+    const size_t work = zero_gamma ? static_cast<size_t>(B) * a.col_len : static_cast<size_t>(B);
+    const size_t blocks = std::min<size_t>((work + 255) / 256, 4096);
+    hipLaunchKernelGGL(k_iac_reset, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s,
+                       const_cast<float *>(a.table), a.cluster_stride, a.col_len, R, B, a.flags, zero_gamma);
+    return hipGetLastError();
+}
+
+template <int R>
+static hipError_t launch_reserve_r(const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
+    if (a.acc128)
+        hipLaunchKernelGGL((k_reserve<R, u128>), grid, block, 0, s, a, ra);
+    else
+        hipLaunchKernelGGL((k_reserve<R, uint64_t>), grid, block, 0, s, a, ra);
+    return hipGetLastError();
+}
+
+hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s) {
+#define CALL(RR) launch_reserve_r<RR>(a, ra, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+}  // namespace esp

@@ -93,17 +93,6 @@ struct KArgs {
 
 constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
 
-// Extra arguments of the effective-capacity kernel (Eq. 12): the KArgs of the
-// pending jobs' context supply the table, the fixed-point windows and the
-// cross-workgroup sum buffers.
-struct ReserveArgs {
-    const uint8_t *queued;         // [B][N] nonzero = pending, or NULL (all pending)
-    const double *cap_phys;        // [B][R] physical capacity C
-    double *cap_eff;               // [B][R] receives C - gamma * S (the active context's capacity)
-    double *out;                   // [B][R] copy for the caller, or NULL
-    double gamma;                  // reservation aggressiveness in [0, 1]
-};
-
 // Host-side launchers (esp_kernels.hip).
 hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 // Cooperative launch (all workgroups co-resident) of a multi-iteration dense launch.
@@ -111,51 +100,6 @@ hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStr
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
-// Arguments of the nearest-profile kernel (RST fallback): queries against
-// the families of a store context (its KArgs supply the table).
-struct NearestArgs {
-    const int32_t *family;         // [B][Q] job type (family index) of each query
-    const float *query;            // [B][Q][R] resource vectors
-    int32_t *nearest;              // [B][Q] index within the family, -1 on error
-    float *estimate;               // [B][Q] utility (throughput) of the nearest entry, or NULL
-    int64_t total;                 // B * Q
-    int32_t Q;                     // queries per cluster
-};
-
-// Outer ESP-IAC rounds (Alg. 1): one wavefront per cluster packs the
-// selection onto GPUs (first fit), evaluates co-located pairs and raises the
-// penalties of offending configurations.
-constexpr int kMaxGpus = 2048;                      // GPUs per cluster (LDS-resident residuals)
-constexpr int kMaxPerGpu = 4;                       // jobs sharing one GPU
-constexpr int kMaxShards = 8;                       // GPUs of one job
-
-struct IacArgs {
-    const int32_t *choice;         // [B][N] selection of this round
-    const int64_t *offsets;        // [N+1] entry offsets of the caller's [B][nnz] arrays
-    int64_t nnz;
-    const int32_t *gpus;           // [B] GPUs per cluster
-    double gpu_memory;             // per-GPU capacity of resource r_mem
-    double gpu_compute;            // per-GPU capacity of resource r_sm
-    int32_t r_gpus, r_mem, r_sm;
-    const float *sensitivity;      // [B][nnz]
-    const float *pressure;         // [B][nnz]
-    const double *tau_base;        // [B][N]
-    double beta, beta_max, u_target, kappa;
-    uint64_t *inc;                 // [B][N] scratch, zero between rounds (bits of doubles >= 0)
-    int32_t *gpu_jobs;             // [B][gmax][kMaxPerGpu] out
-    int32_t gmax;
-    int32_t *rounds_used;          // [B] out
-    int32_t *violations;           // [B] out
-    int32_t round;                 // 1-based
-};
-
-hipError_t launch_pack_iac(int R, const KArgs &a, const IacArgs &m, int B, hipStream_t s);
-// Gamma <- 0 (interference penalties; the switching-cost marks stay) when
-// zero_gamma, and clear the frozen flags.
-hipError_t launch_iac_reset(int R, const KArgs &a, int B, int zero_gamma, hipStream_t s);
-
-hipError_t launch_nearest(int R, const KArgs &a, const NearestArgs &na, hipStream_t s);
-hipError_t launch_reserve(int R, const KArgs &a, const ReserveArgs &ra, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,
                           uint32_t *epoch, int32_t *status, int B, hipStream_t s);
