@@ -93,7 +93,7 @@ def _cpu_baseline(inst, budget_s: float) -> dict:
 def main() -> int:
     args = _parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); "
               "the path shards over jobs but no multi-GPU code is built", file=sys.stderr)
         return 2
     import numpy as np

@@ -9,7 +9,9 @@
  *     lambda_r <- max(0, lambda_r + eta_t (U_r - C_r)),  U_r = sum_j d_{j,c_j,r},
  * with eta_t = eta0 (fixed) or eta0 / sqrt(t), and the loop repeats
  * (Sec. 3.2.3; Alg. 1 "EspTatonnement" followed by a re-selection at the
- * final prices).
+ * final prices).  Around that loop: the penalty Gamma of the ESP score
+ * (Eq. 7), the effective capacity of Eq. 12, the outer ESP-IAC rounds of
+ * Alg. 1 (esp_schedule) and RST's nearest-profile fallback (Sec. 3.1.2).
  *
  * Conventions for every entry point:
  *   - Every function returns an esp_status; nothing aborts or throws.
@@ -17,8 +19,10 @@
  *     caller-owned device memory (any hipMalloc'ed or torch-allocated buffer)
  *     that must stay valid until the work queued on the stream has finished.
  *   - `stream` is a hipStream_t (NULL = the null stream).  Calls other than
- *     esp_create, esp_device_status and esp_destroy only enqueue work: they
- *     return before the GPU has run it.
+ *     esp_create, esp_device_status, esp_read_penalties, esp_schedule (these
+ *     wait for the GPU, as their descriptions say), esp_loop_driver (host
+ *     only) and esp_destroy only enqueue work: they return before the GPU
+ *     has run it.
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - Arithmetic: scores in binary64 in a fixed order without fused
  *     multiply-add: rent = d_0*l_0, rent = rent + d_r*l_r (r = 1..R-1),
@@ -176,9 +180,10 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
 
 /*
  * esp_solve: `iters` iterations t = t_start .. t_start+iters-1 of
- * select -> demand -> update, one fused kernel per iteration (the update runs
- * in the last workgroup of each cluster), then a re-selection at the final
- * prices (Alg. 1).
+ * select -> demand -> update, one fused kernel pass per iteration (the update
+ * runs in the last workgroup of each cluster; the passes run as one launch
+ * each or inside one persistent launch, see ESP_MODE_*), then a re-selection
+ * at the final prices (Alg. 1).
  *   prices      device [B][R], in lambda^{t_start} (finite, >= 0), out the final prices
  *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
  *   tol         0 = run all T iterations; > 0 = a cluster stops after the first
@@ -199,7 +204,9 @@ esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_star
  * error the GPU recorded since the last call: ESP_ERR_NONFINITE or
  * ESP_ERR_INVALID_ARG for prices that were NaN, infinite or negative (the
  * affected calls left prices and outputs unchanged), ESP_ERR_INVALID_ARG for
- * a choice index outside its family; ESP_OK otherwise.
+ * a choice index outside its family, the query errors of
+ * esp_nearest_profile, or a persistent launch whose workgroups waited too
+ * long for each other (ESP_ERR_DEVICE); ESP_OK otherwise.
  */
 esp_status esp_device_status(esp_ctx *ctx, void *stream);
 
