@@ -30,7 +30,9 @@
  *     is the lowest configuration index among equal best scores.  U_r is the
  *     exact sum of the chosen fp32 demands rounded once to binary64
  *     (round-to-nearest-even), so results do not depend on launch geometry.
- *     Step sizes are computed on the host with IEEE division and square root.
+ *     Step sizes eta0 / sqrt(t) are one IEEE division and one correctly
+ *     rounded square root in binary64 (computed on the device from t, so a
+ *     solve holds no host-side state and can be captured in a graph).
  *   - Errors found by the GPU (bad prices, bad choice indices) are recorded
  *     in the context and reported by esp_device_status.
  */
@@ -186,6 +188,10 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
  * at the final prices (Alg. 1).
  *   prices      device [B][R], in lambda^{t_start} (finite, >= 0), out the final prices
  *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
+ * Graph capture: while `stream` is being captured, the iterations are
+ * recorded as one launch each (ESP_MODE_AUTO falls back to it;
+ * ESP_MODE_PERSISTENT returns ESP_ERR_INVALID_ARG); a replay recomputes the
+ * same iterations on the buffers given at capture.
  *   tol         0 = run all T iterations; > 0 = a cluster stops after the first
  *               update with |lambda^{t+1}_r - lambda^t_r| <= tol * max(1, lambda^t_r)
  *               for every r (its later iterations do nothing)

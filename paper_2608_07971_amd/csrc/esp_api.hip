@@ -144,7 +144,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_jobs = o;  o = align_up(o + (pl->csr ? static_cast<size_t>(pl->N) * sizeof(JobSlot) : 0));
     pl->o_shift = o; o = align_up(o + B * R * sizeof(int32_t));
     pl->o_cap = o;   o = align_up(o + B * R * sizeof(double));
-    pl->o_eta = o;   o = align_up(o + B * kEtaChunk * sizeof(double));
+    pl->o_eta = o;   o = align_up(o + B * sizeof(double));
     pl->o_part = o;  o = align_up(o + B * pl->nblk * R * 2 * sizeof(uint64_t));
     pl->o_tick = o;  o = align_up(o + B * sizeof(uint32_t));
     pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
@@ -193,9 +193,9 @@ struct esp_ctx {
     int rule = 0;
     std::vector<double> eta0;
     char *ws = nullptr;
-    double *h_eta = nullptr;           // pinned staging for step sizes
-    hipEvent_t eta_ev = nullptr;
-    bool eta_pending = false;
+    double *h_stage = nullptr;         // pinned staging for capacities and GPU counts
+    hipEvent_t stage_ev = nullptr;     // recorded after the last copy out of h_stage
+    bool stage_pending = false;
     int sweep = 0;                     // 0: alternate the sweep direction, 1: always forward
     int mode = ESP_MODE_AUTO;
     bool auto_mode = false;            // the caller asked for ESP_MODE_AUTO
@@ -255,26 +255,12 @@ esp_status check_ctx(const esp_ctx *c) {
 
 esp_status dev(hipError_t e) { return e == hipSuccess ? ESP_OK : ESP_ERR_DEVICE; }
 
-// Stage step sizes eta_t for t = t0 .. t0+n-1 (n <= kEtaChunk) into the
-// workspace table row-major [i][b].  IEEE division and square root on the host.
-esp_status stage_eta(esp_ctx *c, int64_t t0, int n, hipStream_t s) {
-    const int B = c->pl.B;
-    if (c->eta_pending) {
-        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
-        c->eta_pending = false;
+// Wait until h_stage may be rewritten.
+esp_status stage_wait(esp_ctx *c) {
+    if (c->stage_pending) {
+        if (hipEventSynchronize(c->stage_ev) != hipSuccess) return ESP_ERR_DEVICE;
+        c->stage_pending = false;
     }
-    for (int i = 0; i < n; ++i) {
-        const double t = static_cast<double>(t0 + i);
-        for (int b = 0; b < B; ++b)
-            c->h_eta[static_cast<size_t>(i) * B + b] =
-                (c->rule == ESP_STEP_INV_SQRT) ? c->eta0[b] / std::sqrt(t) : c->eta0[b];
-    }
-    double *d_eta = reinterpret_cast<double *>(c->ws + c->pl.o_eta);
-    if (hipMemcpyAsync(d_eta, c->h_eta, sizeof(double) * static_cast<size_t>(n) * B, hipMemcpyHostToDevice, s) !=
-        hipSuccess)
-        return ESP_ERR_DEVICE;
-    if (hipEventRecord(c->eta_ev, s) != hipSuccess) return ESP_ERR_DEVICE;
-    c->eta_pending = true;
     return ESP_OK;
 }
 
@@ -407,14 +393,14 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
         static_cast<size_t>(B) * pl.columns() * pl.col_len * sizeof(float) > ESP_AUTO_PERSISTENT_BYTES)
         c->mode = ESP_MODE_STREAM;
     auto fail = [&](esp_status e) {
-        if (c->h_eta) (void)hipHostFree(c->h_eta);
-        if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
+        if (c->h_stage) (void)hipHostFree(c->h_stage);
+        if (c->stage_ev) (void)hipEventDestroy(c->stage_ev);
         delete c;
         return e;
     };
-    if (hipHostMalloc(reinterpret_cast<void **>(&c->h_eta), sizeof(double) * B * kEtaChunk) != hipSuccess)
+    if (hipHostMalloc(reinterpret_cast<void **>(&c->h_stage), sizeof(double) * B * kMaxR) != hipSuccess)
         return fail(ESP_ERR_DEVICE);
-    if (hipEventCreateWithFlags(&c->eta_ev, hipEventDisableTiming) != hipSuccess) return fail(ESP_ERR_DEVICE);
+    if (hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming) != hipSuccess) return fail(ESP_ERR_DEVICE);
 
     // ---- pack the table: one column at a time through two pinned buffers ----
     std::vector<TileMeta> meta;
@@ -498,6 +484,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                       hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_capp, cap.data(), sizeof(double) * cap.size(), hipMemcpyHostToDevice,
                                  s) == hipSuccess &&
+                  hipMemcpyAsync(ws + pl.o_eta, c->eta0.data(), sizeof(double) * B, hipMemcpyHostToDevice, s) ==
+                      hipSuccess &&
                   hipMemsetAsync(ws + pl.o_tick, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
@@ -532,7 +520,9 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.tiles = pl.tiles;
     k.nblk = pl.nblk;
     k.cap = reinterpret_cast<const double *>(ws + pl.o_cap);
-    k.eta = reinterpret_cast<const double *>(ws + pl.o_eta);
+    k.eta0 = reinterpret_cast<const double *>(ws + pl.o_eta);
+    k.rule = c->rule == ESP_STEP_INV_SQRT ? 1 : 0;
+    k.t = 1;
     k.shift = reinterpret_cast<const int32_t *>(ws + pl.o_shift);
     k.partials = reinterpret_cast<uint64_t *>(ws + pl.o_part);
     k.tickets = reinterpret_cast<uint32_t *>(ws + pl.o_tick);
@@ -582,8 +572,8 @@ esp_status esp_update_prices(esp_ctx *c, const double *demand, int32_t t, double
     if (st != ESP_OK) return st;
     if (demand == nullptr || prices == nullptr || t < 1) return ESP_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if ((st = stage_eta(c, t, 1, s)) != ESP_OK) return st;
     KArgs a = c->base;
+    a.t = t;
     a.lam_in = prices;
     a.lam_out = prices;
     return dev(launch_update(c->pl.R, a, demand, c->pl.B, s));
@@ -602,13 +592,19 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.epoch, c->base.status, B, s))) != ESP_OK)
         return st;
     // Persistent launches (one cooperative launch per chunk of up to
-    // kEtaChunk iterations); one launch per iteration in stream mode, or when
-    // the device cannot hold the grid co-resident.
-    bool persistent = !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
-    for (int32_t i0 = 0; i0 < iters; i0 += kEtaChunk) {
-        const int n = std::min<int32_t>(kEtaChunk, iters - i0);
-        if ((st = stage_eta(c, static_cast<int64_t>(t_start) + i0, n, s)) != ESP_OK) return st;
+    // kLaunchChunk iterations); one launch per iteration in stream mode, when
+    // the device cannot hold the grid co-resident, or while `stream` is being
+    // captured into a graph (a cooperative launch cannot be captured).
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
+    bool persistent =
+        !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
+    for (int32_t i0 = 0; i0 < iters; i0 += kLaunchChunk) {
+        const int n = std::min<int32_t>(kLaunchChunk, iters - i0);
         KArgs a = c->base;
+        a.t = t_start + i0;
         a.lam_in = prices;
         a.lam_out = prices;
         a.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
@@ -636,7 +632,7 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
         for (int i = 0; i < n; ++i) {
             KArgs ai = a;
             ai.n_iters = 1;
-            ai.eta = c->base.eta + static_cast<size_t>(i) * B;
+            ai.t = t_start + i0 + i;
             ai.iter_no = i0 + i + 1;
             ai.reverse = (c->sweep == 0) ? static_cast<int32_t>((i0 + i) & 1) : 0;
             if (ai.tr_lam) ai.tr_lam = a.tr_lam + static_cast<size_t>(i) * B * R;
@@ -713,18 +709,15 @@ esp_status esp_set_capacity(esp_ctx *c, const double *capacity, void *stream) {
         if (std::fabs(capacity[i]) > 0x1p200) return ESP_ERR_RANGE;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // Stage through the pinned step-size buffer (B * kEtaChunk >= B * R doubles).
-    if (c->eta_pending) {
-        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
-        c->eta_pending = false;
-    }
-    std::memcpy(c->h_eta, capacity, sizeof(double) * n);
-    if (hipMemcpyAsync(c->ws + c->pl.o_capp, c->h_eta, sizeof(double) * n, hipMemcpyHostToDevice, s) != hipSuccess ||
+    // Stage through the pinned buffer (B * kMaxR doubles).
+    if ((st = stage_wait(c)) != ESP_OK) return st;
+    std::memcpy(c->h_stage, capacity, sizeof(double) * n);
+    if (hipMemcpyAsync(c->ws + c->pl.o_capp, c->h_stage, sizeof(double) * n, hipMemcpyHostToDevice, s) != hipSuccess ||
         hipMemcpyAsync(c->ws + c->pl.o_cap, c->ws + c->pl.o_capp, sizeof(double) * n, hipMemcpyDeviceToDevice, s) !=
             hipSuccess ||
-        hipEventRecord(c->eta_ev, s) != hipSuccess)
+        hipEventRecord(c->stage_ev, s) != hipSuccess)
         return ESP_ERR_DEVICE;
-    c->eta_pending = true;
+    c->stage_pending = true;
     return ESP_OK;
 }
 
@@ -798,13 +791,10 @@ esp_status esp_schedule(esp_ctx *c, const esp_iac_model *m, int32_t max_rounds, 
         gmax = std::max(gmax, m->gpus[b]);
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // The pinned step-size buffer stages the GPU counts and reads back the
-    // violation counts between rounds (nothing else uses it meanwhile).
-    if (c->eta_pending) {
-        if (hipEventSynchronize(c->eta_ev) != hipSuccess) return ESP_ERR_DEVICE;
-        c->eta_pending = false;
-    }
-    int32_t *h32 = reinterpret_cast<int32_t *>(c->h_eta);
+    // The pinned staging buffer carries the GPU counts and reads back the
+    // violation counts between rounds (B * kMaxR doubles >= B int32).
+    if ((st = stage_wait(c)) != ESP_OK) return st;
+    int32_t *h32 = reinterpret_cast<int32_t *>(c->h_stage);
     std::memcpy(h32, m->gpus, sizeof(int32_t) * B);
     int32_t *d_gpus = reinterpret_cast<int32_t *>(c->ws + c->pl.o_gpus);
     if (hipMemcpyAsync(d_gpus, h32, sizeof(int32_t) * B, hipMemcpyHostToDevice, s) != hipSuccess ||
@@ -887,9 +877,9 @@ esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {
 esp_status esp_destroy(esp_ctx *c) {
     esp_status st = check_ctx(c);
     if (st != ESP_OK) return st;
-    if (c->eta_pending) (void)hipEventSynchronize(c->eta_ev);
-    if (c->eta_ev) (void)hipEventDestroy(c->eta_ev);
-    if (c->h_eta) (void)hipHostFree(c->h_eta);
+    if (c->stage_pending) (void)hipEventSynchronize(c->stage_ev);
+    if (c->stage_ev) (void)hipEventDestroy(c->stage_ev);
+    if (c->h_stage) (void)hipHostFree(c->h_stage);
     c->magic = 0;
     delete c;
     return ESP_OK;

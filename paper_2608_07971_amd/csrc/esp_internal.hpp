@@ -16,7 +16,7 @@ constexpr int kBlockThreads = 256;                  // 4 wavefronts per workgrou
 constexpr int kBlockWaves = kBlockThreads / kWaveSize;
 constexpr int kMaxR = 8;
 constexpr int kMaxFamily = 256;                     // configurations per job
-constexpr int kEtaChunk = 1024;                     // iterations of step sizes staged at once
+constexpr int kLaunchChunk = 1024;                  // iterations per persistent launch
 
 // Flags per cluster (device int32).
 constexpr int kFlagStopped = 1;                     // converged under tol: skip further updates
@@ -58,7 +58,9 @@ struct KArgs {
     const double *lam_in;          // [B][R] prices at which to select
     double *lam_out;               // [B][R] updated prices, or NULL (no update)
     const double *cap;             // [B][R] capacities
-    const double *eta;             // [B] step sizes of this iteration (when lam_out != NULL)
+    const double *eta0;            // [B] step-size scale eta0 of Eq. 8
+    int32_t rule;                  // 0: eta_t = eta0, 1: eta_t = eta0 / sqrt(t)
+    int32_t t;                     // step index t (1-based) of the launch's first iteration
     const int32_t *shift;          // [B][R] fixed-point window (lowest bit exponent) per column
     uint64_t *partials;            // [B][nblk][R][2] per-workgroup 128-bit sums
     uint32_t *tickets;             // [B] arrival counters (0 between launches)
@@ -76,7 +78,7 @@ struct KArgs {
     int32_t reduce;                // 0: select only (no demand, no ticket)
     int32_t reverse;               // sweep tiles back to front (iteration 0 of the launch)
     int32_t acc128;                // demand accumulators are 128-bit (else 64-bit)
-    // Persistent launches run n_iters iterations; rows of eta / traces / the
+    // Persistent launches run n_iters iterations; t, rows of the traces and the
     // per-iteration choice advance by B, B*R and B*N per iteration, and the
     // sweep direction alternates.  epoch[b] counts finished iterations.
     int32_t n_iters;               // 1 for a single-iteration launch

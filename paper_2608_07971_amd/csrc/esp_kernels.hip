@@ -28,6 +28,14 @@ namespace esp {
 // Cluster completion: per-workgroup sums -> last workgroup -> U, Eq. 8 update
 // ---------------------------------------------------------------------------
 
+// eta_t of Eq. 8 for the launch's step index t: eta0 or eta0 / sqrt(t), one
+// IEEE division and one correctly rounded square root in binary64 (no fast
+// math), so the value equals the host's.
+__device__ __forceinline__ double step_size(const KArgs &a, int cl) {
+    const double e0 = a.eta0[cl];
+    return a.rule == 1 ? e0 / sqrt(static_cast<double>(a.t)) : e0;
+}
+
 // U_r from the cluster's exact total, the Eq. 8 update and the stop test for
 // resource r (one thread per resource of the cluster's last workgroup).
 template <int R>
@@ -41,7 +49,7 @@ __device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r,
     if (a.lam_out) {
         const double lo = a.lam_in[cl * R + r];
         const double g = U - a.cap[cl * R + r];
-        const double x = lo + a.eta[cl] * g;
+        const double x = lo + step_size(a, cl) * g;
         const double ln = (x > 0.0) ? x : 0.0;
         // agent-scope exchange: visible at the coherence point to the other
         // workgroups of a persistent launch once it has returned
@@ -102,7 +110,7 @@ template <int R>
 __device__ __forceinline__ KArgs iteration_args(const KArgs &a, int it) {
     KArgs ai = a;
     const size_t i = static_cast<size_t>(it);
-    ai.eta = a.eta + i * a.B;
+    ai.t = a.t + it;
     if (a.tr_lam) ai.tr_lam = a.tr_lam + i * a.B * R;
     if (a.tr_U) ai.tr_U = a.tr_U + i * a.B * R;
     if (a.choice) ai.choice = a.choice + i * a.B * a.N;
@@ -647,7 +655,7 @@ __global__ void k_update(KArgs a, const double *demand_in, int B) {
     for (int r = 0; r < R; ++r) {
         const double lo = a.lam_in[cl * R + r];
         const double g = demand_in[cl * R + r] - a.cap[cl * R + r];
-        const double x = lo + a.eta[cl] * g;
+        const double x = lo + step_size(a, cl) * g;
         a.lam_out[cl * R + r] = (x > 0.0) ? x : 0.0;
     }
 }
