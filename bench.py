@@ -53,6 +53,9 @@ def _parse():
     ap.add_argument("--nearest", type=int, default=0, metavar="Q",
                     help="instead of the default line: Q nearest-profile queries (RST fallback) against the "
                          "Ragged table used as the profile store; prints queries/s and the gather roofline")
+    ap.add_argument("--store-layout", choices=("aos", "soa"), default="aos",
+                    help="profile-store layout of --nearest: the entry-major copy (ESP_OPT_PROFILE_STORE, "
+                         "default) or the structure-of-arrays columns of the price loop")
     ap.add_argument("--schedule", default="", metavar="CONFIG",
                     help="instead of the default line: Alg. 1 outer rounds (tatonnement, first-fit BinPack, "
                          "co-located pair checks, penalty updates) on CONFIG; --iters per round (default 5), "
@@ -285,7 +288,8 @@ def _nearest(args, esp, workloads, np, torch) -> int:
     fam_np, q_np = workloads.nn_queries(store, args.nearest, seed=9)
     fam = torch.from_numpy(fam_np).cuda()
     q = torch.from_numpy(q_np).cuda()
-    s = esp.Solver(store, mode=args.mode)
+    flags = esp.ESP_OPT_PROFILE_STORE if args.store_layout == "aos" else 0
+    s = esp.Solver(store, mode=args.mode, flags=flags)
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         for _ in range(max(1, args.warmup)):
@@ -311,7 +315,8 @@ def _nearest(args, esp, workloads, np, torch) -> int:
         "value": Q / per_call, "unit": "queries/s", "higher_is_better": True,
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "dtype": "f64", "data": "synthetic",
         "config": {"workload": f"store: Ragged table ({store.N} job types, {store.nnz} profiles, R={R}); "
-                               f"{Q} queries, uniform job type, log-normal(0.25) perturbation, 10% exact hits"},
+                               f"{Q} queries, uniform job type, log-normal(0.25) perturbation, 10% exact hits",
+                   "store_layout": args.store_layout},
         "ms_per_step": per_call * 1e3,
         "roofline": {"bound": "hbm", "achieved": bytes_per_call / per_call / 1e9, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": bytes_per_call / per_call / 1e9 / HBM_PEAK_GBS, "traffic": None,

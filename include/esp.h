@@ -122,8 +122,16 @@ typedef struct {
                                         the memory-side cache), 1 = always front to back; results are
                                         identical either way */
     int32_t mode;                    /* ESP_MODE_* loop driver of esp_solve */
-    int32_t reserved[5];             /* must be zero */
+    int32_t flags;                   /* 0 or ESP_OPT_PROFILE_STORE */
+    int32_t reserved[4];             /* must be zero */
 } esp_options;
+
+/* esp_options.flags: also keep an entry-major copy of the table (each
+ * configuration's utility and R demands contiguous, 4 (1 + R) bytes, so
+ * B * nnz * 4 (1 + R) more workspace bytes) for esp_nearest_profile, which
+ * then reads each job type's family as one contiguous run instead of a piece
+ * of each of the 1 + R columns. */
+#define ESP_OPT_PROFILE_STORE 1
 
 /* Optional per-iteration record of esp_solve (device pointers, iteration-major;
  * row i describes iteration t = t_start + i).  Any field may be NULL. */
@@ -136,7 +144,8 @@ typedef struct {
 /*
  * esp_workspace_size: device workspace bytes esp_create needs for `problem`
  * (only its shapes and offsets are read).  `options` may be NULL.
- * Errors: ESP_ERR_INVALID_ARG (NULL problem/bytes, reserved options nonzero),
+ * Errors: ESP_ERR_INVALID_ARG (NULL problem/bytes, unknown flags or reserved
+ * options nonzero),
  * ESP_ERR_SHAPE.
  */
 esp_status esp_workspace_size(const esp_problem *problem, const esp_options *options, size_t *bytes);

@@ -35,6 +35,7 @@ ESP_STEP_INV_SQRT = 1
 ESP_MODE_AUTO = 0
 ESP_MODE_STREAM = 1
 ESP_MODE_PERSISTENT = 2
+ESP_OPT_PROFILE_STORE = 1
 
 
 class EspError(RuntimeError):
@@ -58,7 +59,7 @@ class esp_step_rule(C.Structure):
 
 class esp_options(C.Structure):
     _fields_ = [("blocks_per_cluster", C.c_int32), ("sweep_order", C.c_int32), ("mode", C.c_int32),
-                ("reserved", C.c_int32 * 5)]
+                ("flags", C.c_int32), ("reserved", C.c_int32 * 4)]
 
 
 class esp_iac_model(C.Structure):
@@ -285,14 +286,14 @@ class Solver:
     dense_k)."""
 
     def __init__(self, inst, device="cuda:0", blocks_per_cluster: int = 0, sweep_order: int = 0,
-                 mode: int = ESP_MODE_AUTO, stream=None):
+                 mode: int = ESP_MODE_AUTO, stream=None, flags: int = 0):
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU: the ESP library has no CPU path")
         self.device = torch.device(device)
         self.problem = Problem.from_instance(inst)
         self.B, self.N, self.R = self.problem.B, self.problem.N, self.problem.R
         self.nnz = int(self.problem.utility.shape[1])
-        self.options = esp_options(int(blocks_per_cluster), int(sweep_order), int(mode))
+        self.options = esp_options(int(blocks_per_cluster), int(sweep_order), int(mode), int(flags))
         nbytes = esp_workspace_size(self.problem, self.options)
         self.workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         with torch.cuda.device(self.device):

@@ -38,9 +38,11 @@ struct Plan {
     int tiles = 0;      // per cluster
     size_t col_len = 0; // floats per column
     int nblk = 0;       // workgroups per cluster
+    int aos_stride = 0; // floats per entry of the entry-major copy, 0 when there is none
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0, total = 0;
+           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
+           o_aos = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -88,7 +90,8 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
         if (opt->blocks_per_cluster < 0) return ESP_ERR_INVALID_ARG;
         if (opt->sweep_order != 0 && opt->sweep_order != 1) return ESP_ERR_INVALID_ARG;
         if (opt->mode < ESP_MODE_AUTO || opt->mode > ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
-        for (int i = 0; i < 5; ++i)
+        if ((opt->flags & ~ESP_OPT_PROFILE_STORE) != 0) return ESP_ERR_INVALID_ARG;
+        for (int i = 0; i < 4; ++i)
             if (opt->reserved[i] != 0) return ESP_ERR_INVALID_ARG;
     }
     if (p->num_clusters < 1 || p->num_jobs < 1 || p->num_resources < 1 || p->num_resources > kMaxR)
@@ -156,6 +159,8 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_offs = o;  o = align_up(o + (static_cast<size_t>(pl->N) + 1) * sizeof(int64_t));
     pl->o_inc = o;   o = align_up(o + B * static_cast<size_t>(pl->N) * sizeof(uint64_t));
     pl->o_gpus = o;  o = align_up(o + B * sizeof(int32_t));
+    if (opt && (opt->flags & ESP_OPT_PROFILE_STORE)) pl->aos_stride = pl->R + 1;
+    pl->o_aos = o;   o = align_up(o + B * static_cast<size_t>(pl->nnz) * pl->aos_stride * sizeof(float));
     pl->total = o;
     return ESP_OK;
 }
@@ -475,6 +480,40 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                 which ^= 1;
             }
         }
+        // Entry-major copy (ESP_OPT_PROFILE_STORE): entry e of cluster b holds
+        // its utility (-inf when masked), then its R demands.
+        if (pl.aos_stride > 0) {
+            const size_t stride = static_cast<size_t>(pl.aos_stride);
+            const size_t per_chunk = std::max<size_t>(1, pp.cap / stride);
+            for (int b = 0; b < B; ++b) {
+                const float *u = p->utility + static_cast<size_t>(b) * nnz;
+                const float *d = p->demand + static_cast<size_t>(b) * nnz * R;
+                const uint8_t *f = p->feasible ? p->feasible + static_cast<size_t>(b) * nnz : nullptr;
+                for (size_t e0 = 0; e0 < static_cast<size_t>(nnz); e0 += per_chunk) {
+                    const size_t n = std::min(per_chunk, static_cast<size_t>(nnz) - e0);
+                    if (pp.pending[which]) {
+                        if (hipEventSynchronize(pp.ev[which]) != hipSuccess) return fail(ESP_ERR_DEVICE);
+                        pp.pending[which] = false;
+                    }
+                    float *h = pp.buf[which];
+                    std::fill(h, h + n * stride, 0.0f);
+                    for (size_t i = 0; i < n; ++i) {
+                        const size_t e = e0 + i;
+                        h[i * stride] = (f && f[e] == 0) ? neg_inf : u[e];
+                        for (int r = 0; r < R; ++r) {
+                            const float v = d[e * R + r];
+                            h[i * stride + 1 + r] = (v == 0.0f) ? 0.0f : v;
+                        }
+                    }
+                    float *dst = reinterpret_cast<float *>(ws + pl.o_aos) + (static_cast<size_t>(b) * nnz + e0) * stride;
+                    if (hipMemcpyAsync(dst, h, sizeof(float) * n * stride, hipMemcpyHostToDevice, s) != hipSuccess ||
+                        hipEventRecord(pp.ev[which], s) != hipSuccess)
+                        return fail(ESP_ERR_DEVICE);
+                    pp.pending[which] = true;
+                    which ^= 1;
+                }
+            }
+        }
         std::vector<double> cap(p->capacity, p->capacity + static_cast<size_t>(B) * R);
         std::vector<double> swc(B, 0.0);
         if (p->switch_cost) swc.assign(p->switch_cost, p->switch_cost + B);
@@ -763,6 +802,11 @@ esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_
     na.estimate = estimate;
     na.total = static_cast<int64_t>(store->pl.B) * num_queries;
     na.Q = num_queries;
+    const Plan &pl = store->pl;
+    na.aos = pl.aos_stride > 0 ? reinterpret_cast<const float *>(store->ws + pl.o_aos) : nullptr;
+    na.offsets = reinterpret_cast<const int64_t *>(store->ws + pl.o_offs);
+    na.nnz = pl.nnz;
+    na.aos_stride = pl.aos_stride;
     return dev(launch_nearest(store->pl.R, store->base, na, static_cast<hipStream_t>(stream)));
 }
 

@@ -146,16 +146,24 @@ __global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs 
 constexpr int kNearestLanes = 16;                     // lanes per query (one DPP row)
 
 // Query i of a cluster names a job type f and an unprofiled configuration's
-// resource vector q.  The 16 lanes of one DPP row serve one query: lane s
-// takes entries s, s+16, ... of family f, skips masked ones (utility -inf),
-// and keeps the smallest squared l2 distance, computed in binary64 in a fixed
+// resource vector q.  The 16 lanes of one DPP row serve a query: lane s takes
+// entries s, s+16, ... of family f, skips masked ones (utility -inf), and
+// keeps the smallest squared l2 distance, computed in binary64 in a fixed
 // order (e_0 = q_0 - d_0, acc = e_0 e_0, acc = acc + e_r e_r for r = 1..R-1).
 // The row then takes the argmax of the negated distance with lowest-index
 // ties (group_argmax), i.e. the nearest entry with the lowest index among
-// equals; lane 0 writes its index and its throughput (the utility column).
-// A family index out of range or a non-finite query component gives -1 /
-// NaN and records an error.
-template <int R>
+// equals.  Lane 0 writes the index; the lane that found the entry writes its
+// throughput (the utility), which it still holds in a register.  A family
+// index out of range or a non-finite query component gives -1 / NaN and
+// records an error.
+//
+// The family is read from the store's entry-major copy (AOS: each entry's
+// utility and demands contiguous, so the family is one contiguous run) or
+// from the structure-of-arrays columns of the price loop's table.  The kernel
+// is bound by the dependent gathers (query -> family extent -> entries), not
+// by its arithmetic; keeping two queries per row in flight was measured
+// slower (fewer resident waves).
+template <int R, bool AOS>
 __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs na) {
     constexpr int kPerBlock = kBlockThreads / kNearestLanes;
     const int sub = threadIdx.x & (kNearestLanes - 1);
@@ -163,50 +171,71 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
     // every lane of a row shares gi, so rows stay whole for the DPP steps
     for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kPerBlock + threadIdx.x / kNearestLanes; gi < na.total;
          gi += stride) {
-        const int cl = static_cast<int>(gi / na.Q);
-        const float *col = a.table + cl * a.cluster_stride;
         const int f = na.family[gi];
-        double q[R];
+        float q[R];
         bool ok = f >= 0 && f < a.N;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            const float v = na.query[gi * R + r];
-            ok = ok && (fabsf(v) <= 3.402823466e38f);     // false for NaN and +-inf
-            q[r] = static_cast<double>(v);
+            q[r] = na.query[gi * R + r];
+            ok = ok && (fabsf(q[r]) <= 3.402823466e38f);     // false for NaN and +-inf
+        }
+        int size = 0;
+        const float *base = nullptr;       // the family's first entry (AOS) or its slot in column 0
+        if (ok) {
+            const int cl = static_cast<int>(gi / na.Q);
+            if constexpr (AOS) {
+                const int64_t e0 = na.offsets[f];
+                size = static_cast<int>(na.offsets[f + 1] - e0);
+                base = na.aos + (static_cast<size_t>(cl) * na.nnz + e0) * na.aos_stride;
+            } else {
+                uint32_t slot;
+                if (a.K > 0) {
+                    slot = static_cast<uint32_t>(f) * static_cast<uint32_t>(a.K);
+                    size = a.K;
+                } else {
+                    slot = a.jobs[f].slot;
+                    size = static_cast<int>(a.jobs[f].size);
+                }
+                base = a.table + cl * a.cluster_stride + slot;
+            }
         }
         double best = -__builtin_inf();
         int bk = 0x7fffffff;
-        uint32_t slot = 0;
-        if (ok) {
-            uint32_t size;
-            if (a.K > 0) {
-                slot = static_cast<uint32_t>(f) * static_cast<uint32_t>(a.K);
-                size = static_cast<uint32_t>(a.K);
+        float bu = 0.0f;
+        for (int k = sub; k < size; k += kNearestLanes) {
+            float d[R + 1];                                  // utility, then the R demands
+            if constexpr (AOS) {
+                __builtin_memcpy(d, base + static_cast<size_t>(k) * na.aos_stride, sizeof d);
             } else {
-                slot = a.jobs[f].slot;
-                size = a.jobs[f].size;
-            }
-            for (uint32_t k = sub; k < size; k += kNearestLanes) {
-                const size_t e = static_cast<size_t>(slot) + k;
-                if (col[e] == -__builtin_inff()) continue;     // masked configuration
-                double x = q[0] - static_cast<double>(col[a.col_len + e]);
-                double acc = x * x;
 #pragma unroll
-                for (int r = 1; r < R; ++r) {
-                    x = q[r] - static_cast<double>(col[(r + 1) * a.col_len + e]);
-                    acc = acc + x * x;
-                }
-                take_better(best, bk, -acc, static_cast<int>(k));
+                for (int r = 0; r <= R; ++r) d[r] = base[r * a.col_len + k];
             }
+            double x = static_cast<double>(q[0]) - static_cast<double>(d[1]);
+            double acc = x * x;
+#pragma unroll
+            for (int r = 1; r < R; ++r) {
+                x = static_cast<double>(q[r]) - static_cast<double>(d[r + 1]);
+                acc = acc + x * x;
+            }
+            // Masked configurations (utility -inf) are no candidates.  k ascends
+            // within a lane, so keeping the first of equal distances keeps the
+            // lowest index.  Selects, not a branch: all of the entry's loads
+            // are issued before the mask is tested.
+            const bool take = d[0] != -__builtin_inff() && -acc > best;
+            best = take ? -acc : best;
+            bk = take ? k : bk;
+            bu = take ? d[0] : bu;
         }
+        const int mine = bk;
         group_argmax<kNearestLanes>(best, bk);
+        const bool found = ok && bk != 0x7fffffff;
         if (sub == 0) {
-            const bool found = ok && bk != 0x7fffffff;
             na.nearest[gi] = found ? bk : -1;
-            if (na.estimate)
-                na.estimate[gi] = found ? col[static_cast<size_t>(slot) + static_cast<uint32_t>(bk)] : __builtin_nanf("");
+            if (na.estimate && !found) na.estimate[gi] = __builtin_nanf("");
             if (!ok) atomicCAS(a.status, 0, (f >= 0 && f < a.N) ? kStatusNonfinite : kStatusInvalid);
         }
+        // the entry's own lane (entries k of lane s satisfy k = s mod 16)
+        if (found && na.estimate && mine == bk) na.estimate[gi] = bu;
     }
 }
 
@@ -482,7 +511,10 @@ static hipError_t launch_nearest_r(const KArgs &a, const NearestArgs &na, hipStr
     const int64_t need = (na.total + kPerBlock - 1) / kPerBlock;
     const int64_t cap = 256 * 32;                    // enough resident queries to cover gather latency
     const dim3 grid(static_cast<unsigned>(need < cap ? need : cap)), block(kBlockThreads);
-    hipLaunchKernelGGL((k_nearest<R>), grid, block, 0, s, a, na);
+    if (na.aos)
+        hipLaunchKernelGGL((k_nearest<R, true>), grid, block, 0, s, a, na);
+    else
+        hipLaunchKernelGGL((k_nearest<R, false>), grid, block, 0, s, a, na);
     return hipGetLastError();
 }
 

@@ -27,6 +27,14 @@ struct NearestArgs {
     float *estimate;               // [B][Q] utility (throughput) of the nearest entry, or NULL
     int64_t total;                 // B * Q
     int32_t Q;                     // queries per cluster
+    // Entry-major copy of the store (ESP_OPT_PROFILE_STORE), or NULL: entry e
+    // of cluster b at aos + (b * nnz + e) * aos_stride, utility first, then
+    // the R demands; entries in the problem's order (family f = offsets[f]
+    // .. offsets[f+1] - 1).
+    const float *aos;
+    const int64_t *offsets;        // [N+1]
+    int64_t nnz;
+    int32_t aos_stride;            // floats per entry: 1 + R
 };
 
 // Outer ESP-IAC rounds (Alg. 1): one wavefront per cluster packs the

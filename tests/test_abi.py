@@ -50,6 +50,17 @@ def test_workspace_size_dense_and_csr():
     assert _ws(esp.Problem.from_instance(L)) >= L.table_bytes()
 
 
+def test_workspace_size_profile_store():
+    # the entry-major copy adds B * nnz * (1 + R) floats (plus alignment)
+    for inst in (workloads.make("tiny"), workloads.make("ragged", n_jobs=3000)):
+        p = esp.Problem.from_instance(inst)
+        base = _ws(p)
+        more = _ws(p, esp.esp_options(0, 0, 0, esp.ESP_OPT_PROFILE_STORE))
+        nnz = int(p.utility.shape[1])
+        extra = p.B * nnz * (p.R + 1) * 4
+        assert extra <= more - base <= extra + 256
+
+
 @pytest.mark.parametrize("field,value,code", [
     ("num_resources", 0, esp.ESP_ERR_SHAPE), ("num_resources", 9, esp.ESP_ERR_SHAPE),
     ("num_jobs", 0, esp.ESP_ERR_SHAPE), ("num_clusters", 0, esp.ESP_ERR_SHAPE),
@@ -76,6 +87,9 @@ def test_bad_offsets_and_options():
     opt2 = esp.esp_options(0, 5)
     with pytest.raises(esp.EspError) as e:
         _ws(p2, opt)
+    assert e.value.code == esp.ESP_ERR_INVALID_ARG
+    with pytest.raises(esp.EspError) as e:
+        _ws(p2, esp.esp_options(0, 0, 0, 2))          # unknown flag
     assert e.value.code == esp.ESP_ERR_INVALID_ARG
     with pytest.raises(esp.EspError):
         _ws(p2, esp.esp_options(-1))

@@ -1,7 +1,9 @@
 """GPU parity of RST's nearest-profile fallback (Sec. 3.1.2, Sec. 4.1)
 through the C-ABI against the oracle: the nearest index is an integer
 decided by binary64 distances computed in the same order on both sides, so
-indices and estimates must be bit-exact."""
+indices and estimates must be bit-exact.  Every case runs on both layouts of
+the store: the structure-of-arrays columns and the entry-major copy
+(ESP_OPT_PROFILE_STORE)."""
 import math
 
 import numpy as np
@@ -27,16 +29,20 @@ def _run(store_solver, fam, q):
     return n.cpu().numpy(), e.cpu().numpy()
 
 
+LAYOUTS = {"soa": 0, "aos": esp.ESP_OPT_PROFILE_STORE}
+
+
 def _check(store, fam, q):
-    s = esp.Solver(store)
-    n, e = _run(s, fam, q)
     o = oracle.Oracle(store)
-    for b in range(store.B):
-        k, est = o.nearest_batch(b, fam[b], q[b])
-        assert np.array_equal(n[b], k), b
-        assert np.array_equal(e[b].view(np.uint32), est.view(np.uint32)), b
-    assert s.device_status() == 0
-    s.close()
+    want = [o.nearest_batch(b, fam[b], q[b]) for b in range(store.B)]
+    for name, flags in LAYOUTS.items():
+        s = esp.Solver(store, flags=flags)
+        n, e = _run(s, fam, q)
+        for b, (k, est) in enumerate(want):
+            assert np.array_equal(n[b], k), (name, b)
+            assert np.array_equal(e[b].view(np.uint32), est.view(np.uint32)), (name, b)
+        assert s.device_status() == 0
+        s.close()
 
 
 def test_hand_example_on_gpu():
@@ -47,10 +53,12 @@ def test_hand_example_on_gpu():
         rows = [r for r in g[key] if 0 <= int(r[0][0]) < store.N]
         fam = np.array([[int(r[0][0]) for r in rows]], np.int32)
         q = np.array([[r[1] for r in rows]], np.float32)
-        s = esp.Solver(store)
-        n, e = _run(s, fam, q)
-        assert list(n[0]) == [int(r[2][0]) for r in rows]
-        assert list(e[0]) == [r[3][0] for r in rows]
+        for flags in LAYOUTS.values():
+            s = esp.Solver(store, flags=flags)
+            n, e = _run(s, fam, q)
+            assert list(n[0]) == [int(r[2][0]) for r in rows]
+            assert list(e[0]) == [r[3][0] for r in rows]
+            s.close()
 
 
 STORES = {
@@ -98,14 +106,15 @@ def test_small_integer_grid_has_many_ties():
     _check(store, fam, q.astype(np.float32))
 
 
-def test_bad_queries_are_reported():
+@pytest.mark.parametrize("layout", sorted(LAYOUTS))
+def test_bad_queries_are_reported(layout):
     store = workloads.random_small(26, 100, 8, 3)
-    s = esp.Solver(store)
+    s = esp.Solver(store, flags=LAYOUTS[layout])
     fam = np.array([[0, -1, 100, 5, 7]], np.int32)
     q = np.ones((1, 5, 3), np.float32)
     q[0, 3, 1] = np.nan
     q[0, 4, 2] = np.inf
-    _say("nearest bad queries")
+    _say(f"nearest bad queries ({layout})")
     n, e = _run(s, fam, q)
     assert list(n[0, 1:]) == [-1, -1, -1, -1] and np.isnan(e[0, 1:]).all()
     assert n[0, 0] == oracle.Oracle(store).nearest(0, 0, q[0, 0])[0]
