@@ -42,7 +42,7 @@ struct Plan {
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
            o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
-           o_aos = 0, total = 0;
+           o_aos = 0, o_lamws = 0, o_conv = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -127,16 +127,23 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
         if (tiles > INT32_MAX / 2) return ESP_ERR_SHAPE;
         pl->tiles = static_cast<int>(tiles);
     }
-    pl->col_len = static_cast<size_t>(pl->tiles) * kTileEntries;
+    // Columns are kColumnPadTiles tiles longer than the table, so that the
+    // 1 + R columns of a cluster do not start at the same offset modulo large
+    // powers of two (one wavefront reads the same tile of every column at
+    // once).  Measured on Large: 93.9 us per pass with the pad, 96.9 without.
+    pl->col_len = (static_cast<size_t>(pl->tiles) + kColumnPadTiles) * kTileEntries;
     if (pl->col_len >= (static_cast<size_t>(1) << 32)) return ESP_ERR_SHAPE;
-    // Workgroups: one per compute unit over the whole device, split across
-    // clusters (a persistent-style grid: every workgroup sweeps many tiles).
+    // Workgroups over the whole device, split across clusters (every
+    // workgroup sweeps many tiles).  The CSR kernel does more VALU work per
+    // tile and runs two workgroups per compute unit.  The dense kernel runs
+    // one per compute unit on three quarters of the units: with every unit
+    // streaming, the workgroups finish further apart and a pass takes longer
+    // (Large: 90 us per pass at 192 workgroups, 94 us at 256).
     const int max_useful = std::max(1, (pl->tiles + kBlockWaves - 1) / kBlockWaves);
     const int cus = device_cus();
-    // The CSR kernel does more VALU work per tile and runs two workgroups per CU.
-    const int per_cu = pl->csr ? 2 : 1;
+    const int total = pl->csr ? 2 * cus : std::max(1, 3 * cus / 4);
     int nblk = (opt && opt->blocks_per_cluster > 0) ? opt->blocks_per_cluster
-                                                     : std::max(1, (per_cu * cus + pl->B - 1) / pl->B);
+                                                     : std::max(1, (total + pl->B - 1) / pl->B);
     pl->nblk = std::min(nblk, max_useful);
     if (static_cast<int64_t>(pl->nblk) * pl->B > INT32_MAX) return ESP_ERR_SHAPE;
 
@@ -148,7 +155,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_shift = o; o = align_up(o + B * R * sizeof(int32_t));
     pl->o_cap = o;   o = align_up(o + B * R * sizeof(double));
     pl->o_eta = o;   o = align_up(o + B * sizeof(double));
-    pl->o_part = o;  o = align_up(o + B * pl->nblk * R * 2 * sizeof(uint64_t));
+    pl->o_part = o;  o = align_up(o + kPartialBuffers * B * pl->nblk * R * 2 * sizeof(uint64_t));
     pl->o_tick = o;  o = align_up(o + B * sizeof(uint32_t));
     pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
     pl->o_iters = o; o = align_up(o + B * sizeof(int32_t));
@@ -161,6 +168,8 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_gpus = o;  o = align_up(o + B * sizeof(int32_t));
     if (opt && (opt->flags & ESP_OPT_PROFILE_STORE)) pl->aos_stride = pl->R + 1;
     pl->o_aos = o;   o = align_up(o + B * static_cast<size_t>(pl->nnz) * pl->aos_stride * sizeof(float));
+    pl->o_lamws = o; o = align_up(o + 2 * B * R * sizeof(double));
+    pl->o_conv = o;  o = align_up(o + B * sizeof(int32_t));
     pl->total = o;
     return ESP_OK;
 }
@@ -529,6 +538,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_epoch, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_conv, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_swc, swc.data(), sizeof(double) * B, hipMemcpyHostToDevice, s) ==
                       hipSuccess &&
                   hipMemsetAsync(ws + pl.o_status, 0, sizeof(int32_t), s) == hipSuccess &&
@@ -572,6 +582,8 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.n_iters = 1;
     k.B = B;
     k.epoch = reinterpret_cast<uint32_t *>(ws + pl.o_epoch);
+    k.lam_ws = reinterpret_cast<double *>(ws + pl.o_lamws);
+    k.conv_at = reinterpret_cast<int32_t *>(ws + pl.o_conv);
     k.sweep_alt = c->sweep == 0 ? 1 : 0;
     *out = c;
     return ESP_OK;
@@ -582,9 +594,9 @@ esp_status esp_score_select(esp_ctx *c, const double *prices, int32_t *choice, v
     if (st != ESP_OK) return st;
     if (prices == nullptr || choice == nullptr) return ESP_ERR_INVALID_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if ((st = dev(launch_prepare(c->pl.R, prices, c->base.flags, nullptr, nullptr, c->base.status, c->pl.B, s))) !=
-        ESP_OK)
-        return st;
+    KArgs p = c->base;
+    p.iters_done = nullptr;
+    if ((st = dev(launch_prepare(c->pl.R, p, prices, c->pl.B, s))) != ESP_OK) return st;
     KArgs a = c->base;
     a.lam_in = prices;
     a.choice = choice;
@@ -628,8 +640,15 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
     int32_t *d_iters = reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters);
-    if ((st = dev(launch_prepare(R, prices, c->base.flags, d_iters, c->base.epoch, c->base.status, B, s))) != ESP_OK)
-        return st;
+    {
+        KArgs p = c->base;
+        p.iters_done = d_iters;
+        if ((st = dev(launch_prepare(R, p, prices, B, s))) != ESP_OK) return st;
+    }
+    // With several workgroups per cluster every iteration only publishes its
+    // sums; the next launch (or the closing one) completes it.  With one
+    // workgroup per cluster the workgroup completes its own iteration.
+    const bool defer = c->pl.nblk > 1;
     // Persistent launches (one cooperative launch per chunk of up to
     // kLaunchChunk iterations); one launch per iteration in stream mode, when
     // the device cannot hold the grid co-resident, or while `stream` is being
@@ -640,26 +659,46 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
     bool persistent =
         !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
+    KArgs base = c->base;
+    base.lam_in = prices;
+    base.lam_dst = prices;
+    base.iters_done = d_iters;
+    base.tol = tol;
+    base.defer = defer ? 1 : 0;
+    if (defer) {
+        base.lam_out = nullptr;
+        base.skip_mask = kFlagError | kFlagFrozen;
+        if (trace) {
+            base.trace_lam = trace->prices;
+            base.trace_U = trace->demand;
+        }
+    } else {
+        base.lam_out = prices;
+        base.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
+    }
+    // Launch arguments for solve iterations i .. i + n - 1 (0-based).
+    auto iteration_launch = [&](int32_t i, int32_t n) {
+        KArgs a = base;
+        a.n_iters = n;
+        a.t = t_start + i;
+        a.iter_no = i + 1;
+        a.reduce = 1;
+        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i & 1) : 0;
+        if (defer && i > 0) {
+            a.pend_m = i;
+            a.pend_t = t_start + i - 1;
+        }
+        if (trace) {
+            if (!defer && trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(i) * B * R;
+            if (!defer && trace->demand) a.tr_U = trace->demand + static_cast<size_t>(i) * B * R;
+            if (trace->choice) a.choice = trace->choice + static_cast<size_t>(i) * B * N;
+        }
+        return a;
+    };
     for (int32_t i0 = 0; i0 < iters; i0 += kLaunchChunk) {
         const int n = std::min<int32_t>(kLaunchChunk, iters - i0);
-        KArgs a = c->base;
-        a.t = t_start + i0;
-        a.lam_in = prices;
-        a.lam_out = prices;
-        a.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
-        a.iters_done = d_iters;
-        a.tol = tol;
-        a.reduce = 1;
-        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i0 & 1) : 0;
-        a.iter_no = i0 + 1;
-        if (trace) {
-            if (trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(i0) * B * R;
-            if (trace->demand) a.tr_U = trace->demand + static_cast<size_t>(i0) * B * R;
-            if (trace->choice) a.choice = trace->choice + static_cast<size_t>(i0) * B * N;
-        }
         if (persistent) {
-            a.n_iters = n;
-            a.epoch_base = static_cast<uint32_t>(i0);
+            const KArgs a = iteration_launch(i0, n);
             const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
                                            : launch_dense_persistent(R, c->pl.lpj, a, B, s);
             if (e == hipSuccess) continue;
@@ -668,28 +707,29 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
             persistent = false;                // fall back to one launch per iteration
             c->fell_back = true;
         }
-        for (int i = 0; i < n; ++i) {
-            KArgs ai = a;
-            ai.n_iters = 1;
-            ai.t = t_start + i0 + i;
-            ai.iter_no = i0 + i + 1;
-            ai.reverse = (c->sweep == 0) ? static_cast<int32_t>((i0 + i) & 1) : 0;
-            if (ai.tr_lam) ai.tr_lam = a.tr_lam + static_cast<size_t>(i) * B * R;
-            if (ai.tr_U) ai.tr_U = a.tr_U + static_cast<size_t>(i) * B * R;
-            if (ai.choice) ai.choice = a.choice + static_cast<size_t>(i) * B * N;
-            if ((st = dev(launch_select(c, ai, s))) != ESP_OK) return st;
-        }
+        for (int i = 0; i < n; ++i)
+            if ((st = dev(launch_select(c, iteration_launch(i0 + i, 1), s))) != ESP_OK) return st;
     }
-    // Re-selection at the final prices (no update).
+    // Closing launch: completes the last iteration of a deferred solve, and
+    // re-selects at the final prices (no update) when asked to.
+    KArgs a = base;
+    a.lam_out = nullptr;
+    a.tr_lam = a.tr_U = nullptr;
+    a.defer = 0;
+    a.n_iters = 1;
+    a.skip_mask = kFlagError | kFlagFrozen;
+    if (defer && iters > 0) {
+        a.pend_m = iters;
+        a.pend_t = t_start + iters - 1;
+    }
     if (choice || demand) {
-        KArgs a = c->base;
-        a.lam_in = prices;
         a.choice = choice;
         a.demand_out = demand;
-        a.skip_mask = kFlagError | kFlagFrozen;
         a.reduce = demand ? 1 : 0;
         a.reverse = (c->sweep == 0) ? static_cast<int32_t>(iters & 1) : 0;
         if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
+    } else if (a.pend_m > 0) {
+        if ((st = dev(launch_finish(R, a, B, s))) != ESP_OK) return st;
     }
     if (iters_done &&
         hipMemcpyAsync(iters_done, d_iters, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s) != hipSuccess)

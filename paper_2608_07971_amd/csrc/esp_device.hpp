@@ -108,20 +108,120 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
     return ldexp(static_cast<double>(m), drop + sh);
 }
 
-// Cross-workgroup exact sums of one cluster.  bsum[r] (LDS) holds this
-// workgroup's 128-bit sum for resource r.  In the workgroup that finishes
-// last, thread r < R runs done(r, total_r) with the cluster's total; the
-// function returns true there (after a workgroup barrier) and false in every
-// other workgroup.
+// Partial-sum buffer k of cluster cl: [nblk][R][2] 64-bit words (low, high).
+template <int R>
+__device__ __forceinline__ uint64_t *partials_of(const KArgs &a, int k, int cl) {
+    return a.partials + (static_cast<size_t>(k) * a.B + cl) * static_cast<size_t>(a.nblk) * R * 2;
+}
+
+// Publish this workgroup's sums bsum[r] (LDS) into buffer k with agent-scope
+// atomic exchanges, which are performed at the device coherence point, and
+// wait until they have completed (their old values are back).  Runs in
+// wavefront 0; the caller orders the rest of the workgroup.
+template <int R>
+__device__ __forceinline__ void publish_sums(const KArgs &a, int k, int cl, int blk, const u128 *bsum) {
+    const int t = threadIdx.x;
+    uint64_t old = 0;
+    if (t < R) {
+        uint64_t *p = partials_of<R>(a, k, cl) + (static_cast<size_t>(blk) * R + t) * 2;
+        const u128 v = bsum[t];
+        old ^= __hip_atomic_exchange(p, static_cast<uint64_t>(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        old ^= __hip_atomic_exchange(p + 1, static_cast<uint64_t>(v >> 64), __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" : : "v"(old) : "memory");
+}
+
+// Totals over the nblk published sums of buffer k.  Thread (g, r), g < G =
+// kBlockThreads / R, takes blocks g, g+G, g+2G, ...: partial_loads issues the
+// first kSumLoads of them (so that a caller can start them early, before
+// other loads), partial_totals loads the rest, adds, and runs a tree over g
+// in LDS; afterwards s_red[r] holds the cluster's total for resource r (all
+// threads take part; ends with a workgroup barrier).  With 64-bit
+// accumulators every sum fits in the low word, the high word is not read.
+// Coherent: agent-scope atomic loads, which bypass the non-coherent caches
+// (sums published in the same launch); otherwise plain loads (sums of an
+// earlier launch, made visible by the launch boundary).
+constexpr int kSumLoads = 8;
+
+template <typename A, bool Coherent>
+__device__ __forceinline__ A load_sum(uint64_t *p) {
+    uint64_t lo, hi = 0;
+    if constexpr (Coherent) {
+        lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if constexpr (sizeof(A) > 8) hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+        lo = p[0];
+        if constexpr (sizeof(A) > 8) hi = p[1];
+    }
+    if constexpr (sizeof(A) > 8) return (static_cast<A>(hi) << 64) | lo;
+    else return static_cast<A>(lo);
+}
+
+// Every thread loads kSumLoads sums without branches (addresses past the
+// last block are clamped to it and the value replaced by zero), so that the
+// compiler can wait for exactly these loads.
+template <int R, typename A, bool Coherent>
+__device__ __forceinline__ void partial_loads(const KArgs &a, int k, int cl, A (&v)[kSumLoads]) {
+    constexpr int G = kBlockThreads / R;
+    const int t = threadIdx.x;
+    const int r = t % R, g = t / R;
+    uint64_t *base = partials_of<R>(a, k, cl) + static_cast<size_t>(r) * 2;
+#pragma unroll
+    for (int u = 0; u < kSumLoads; ++u) {
+        const int b = g + u * G;
+        const A x = load_sum<A, Coherent>(base + static_cast<size_t>(min(b, a.nblk - 1)) * R * 2);
+        v[u] = (t < G * R && b < a.nblk) ? x : A(0);
+    }
+}
+
+template <int R, typename A, bool Coherent>
+__device__ __forceinline__ void partial_totals(const KArgs &a, int k, int cl, const A (&v)[kSumLoads],
+                                               u128 *s_red) {
+    constexpr int G = kBlockThreads / R;
+    const int t = threadIdx.x;
+    u128 s = 0;
+#pragma unroll
+    for (int u = 0; u < kSumLoads; ++u) s += static_cast<u128>(v[u]);
+    if (t < G * R) {
+        const int r = t % R, g = t / R;
+        uint64_t *base = partials_of<R>(a, k, cl) + static_cast<size_t>(r) * 2;
+#pragma unroll 1
+        for (int b0 = g + kSumLoads * G; b0 < a.nblk; b0 += kSumLoads * G) {
+            A w[kSumLoads];
+#pragma unroll
+            for (int u = 0; u < kSumLoads; ++u) {
+                const int b = b0 + u * G;
+                w[u] = b < a.nblk ? load_sum<A, Coherent>(base + static_cast<size_t>(b) * R * 2) : A(0);
+            }
+#pragma unroll
+            for (int u = 0; u < kSumLoads; ++u) s += static_cast<u128>(w[u]);
+        }
+    }
+    s_red[t] = s;
+    __syncthreads();
+    // tree over the G groups (integer adds: the order does not matter)
+#pragma unroll
+    for (int h = 128; h >= 1; h >>= 1) {
+        if (h < G) {
+            if (t < h * R && t + h * R < G * R) s_red[t] += s_red[t + h * R];
+            __syncthreads();
+        }
+    }
+}
+
+// Cross-workgroup exact sums of one cluster within one launch.  bsum[r]
+// (LDS) holds this workgroup's 128-bit sum for resource r.  In the workgroup
+// that finishes last, thread r < R runs done(r, total_r) with the cluster's
+// total; the function returns true there (after a workgroup barrier) and
+// false in every other workgroup.
 //
 // Ordering across the 8 XCDs (each with its own L2) without cache-wide
-// writeback or invalidation: wavefront 0 publishes the partial with
-// agent-scope atomic exchanges, which are performed at the device coherence
-// point and have completed once their old values are back; it waits for them
-// (s_waitcnt vmcnt(0) on the returned values) before it takes a ticket with
-// an agent-scope atomic add.  The workgroup that draws the last ticket reads
-// every partial with agent-scope atomic loads, which bypass the non-coherent
-// caches, and resets the ticket for the next use.
+// writeback or invalidation: the sums are published with agent-scope atomic
+// exchanges that have completed before the workgroup takes a ticket with an
+// agent-scope atomic add.  The workgroup that draws the last ticket reads
+// every sum with agent-scope atomic loads and resets the ticket for the next
+// use.
 template <int R, typename Done>
 __device__ __forceinline__ bool cluster_sums(const KArgs &a, int cl, int blk, const u128 *bsum, Done &&done) {
     __shared__ int s_last;
@@ -136,15 +236,7 @@ __device__ __forceinline__ bool cluster_sums(const KArgs &a, int cl, int blk, co
         return true;
     }
     if (t < kWaveSize) {
-        uint64_t old = 0;
-        if (t < R) {
-            uint64_t *p = a.partials + ((static_cast<size_t>(cl) * a.nblk + blk) * R + t) * 2;
-            const u128 v = bsum[t];
-            old ^= __hip_atomic_exchange(p, static_cast<uint64_t>(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            old ^= __hip_atomic_exchange(p + 1, static_cast<uint64_t>(v >> 64), __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
-        }
-        asm volatile("s_waitcnt vmcnt(0)" : : "v"(old) : "memory");
+        publish_sums<R>(a, kInLaunchBuffer, cl, blk, bsum);
         if (t == 0) {
             const unsigned prev = __hip_atomic_fetch_add(&a.tickets[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             s_last = (prev == static_cast<unsigned>(a.nblk) - 1u);
@@ -152,41 +244,10 @@ __device__ __forceinline__ bool cluster_sums(const KArgs &a, int cl, int blk, co
     }
     __syncthreads();
     if (!s_last) return false;
-
-    // Sum the nblk partials of each resource: thread (g, r) takes blocks
-    // g, g+G, g+2G, ...; eight independent loads in flight per thread.
-    constexpr int G = kBlockThreads / R;
-    constexpr int U = 8;
-    u128 s = 0;
-    if (t < G * R) {
-        const int r = t % R, g = t / R;
-        const uint64_t *base = a.partials + (static_cast<size_t>(cl) * a.nblk * R + r) * 2;
-#pragma unroll 1
-        for (int b0 = g; b0 < a.nblk; b0 += U * G) {
-            u128 v[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int b = b0 + u * G;
-                v[u] = 0;
-                if (b < a.nblk) {
-                    uint64_t *p = const_cast<uint64_t *>(base) + static_cast<size_t>(b) * R * 2;
-                    const uint64_t lo = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const uint64_t hi = __hip_atomic_load(p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    v[u] = (static_cast<u128>(hi) << 64) | lo;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) s += v[u];
-        }
-    }
-    s_red[t] = s;
-    __syncthreads();
-    if (t < R) {
-        u128 tot = 0;
-#pragma unroll 1
-        for (int g = 0; g < G; ++g) tot += s_red[g * R + t];
-        done(t, tot);
-    }
+    u128 v[kSumLoads];
+    partial_loads<R, u128, true>(a, kInLaunchBuffer, cl, v);
+    partial_totals<R, u128, true>(a, kInLaunchBuffer, cl, v, s_red);
+    if (t < R) done(t, s_red[t]);
     if (t == 0) {
         // ready for the next use
         const unsigned o = __hip_atomic_exchange(&a.tickets[cl], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

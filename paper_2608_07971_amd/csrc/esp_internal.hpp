@@ -17,6 +17,11 @@ constexpr int kBlockWaves = kBlockThreads / kWaveSize;
 constexpr int kMaxR = 8;
 constexpr int kMaxFamily = 256;                     // configurations per job
 constexpr int kLaunchChunk = 1024;                  // iterations per persistent launch
+constexpr int kColumnPadTiles = 7;                  // unused tiles at the end of every column
+// Buffers of per-workgroup sums: 0 and 1 hold the sums of solve iterations by
+// iteration parity (deferred completion), 2 those of in-launch completion.
+constexpr int kPartialBuffers = 3;
+constexpr int kInLaunchBuffer = 2;
 
 // Flags per cluster (device int32).
 constexpr int kFlagStopped = 1;                     // converged under tol: skip further updates
@@ -62,7 +67,7 @@ struct KArgs {
     int32_t rule;                  // 0: eta_t = eta0, 1: eta_t = eta0 / sqrt(t)
     int32_t t;                     // step index t (1-based) of the launch's first iteration
     const int32_t *shift;          // [B][R] fixed-point window (lowest bit exponent) per column
-    uint64_t *partials;            // [B][nblk][R][2] per-workgroup 128-bit sums
+    uint64_t *partials;            // [kPartialBuffers][B][nblk][R][2] per-workgroup 128-bit sums
     uint32_t *tickets;             // [B] arrival counters (0 between launches)
     int32_t *flags;                // [B] per-cluster run flags
     int32_t skip_mask;             // skip a cluster when (flags[b] & skip_mask) != 0
@@ -80,17 +85,31 @@ struct KArgs {
     int32_t acc128;                // demand accumulators are 128-bit (else 64-bit)
     // Persistent launches run n_iters iterations; t, rows of the traces and the
     // per-iteration choice advance by B, B*R and B*N per iteration, and the
-    // sweep direction alternates.  epoch[b] counts finished iterations.
+    // sweep direction alternates.
     int32_t n_iters;               // 1 for a single-iteration launch
     int32_t B;                     // clusters
-    uint32_t *epoch;               // [B] (persistent launches)
-    uint32_t epoch_base;           // epoch value when this launch starts
+    uint32_t *epoch;               // [B] workgroup arrivals of deferred iterations (reset per solve)
     int32_t sweep_alt;             // alternate the sweep direction between iterations
     // Penalty of the ESP score (Eq. 7): column R + 1 of each cluster holds
     // |penalty| per entry, its sign bit set when the entry is not the job's
     // current configuration (the switching cost switch_cost[b] applies).
     int32_t has_pen;
     const double *switch_cost;     // [B]
+    // Deferred completion of solve iterations (several workgroups per
+    // cluster).  Iteration m (1-based within the solve: iter_no) publishes the
+    // workgroup sums into partials buffer m & 1 and ends there.  U_m,
+    // lambda_{m+1} and the stop test are computed by every workgroup of the
+    // cluster from those sums when iteration m + 1 (or the closing launch)
+    // starts.  The sums are integers, so every workgroup obtains the same
+    // bits; workgroup 0 writes the outputs.
+    int32_t defer;                 // this launch's iterations publish their sums only
+    int32_t pend_m;                // > 0: first complete iteration pend_m of the solve
+    int32_t pend_t;                // its step index t
+    double *lam_ws;                // [2][B][R] lambda_m of iteration m at index m & 1
+    double *lam_dst;               // [B][R] the caller's prices: receives every lambda_{m+1}
+    int32_t *conv_at;              // [B] iteration whose completion met tol, 0 while none has
+    double *trace_lam;             // [iters][B][R]: row m - 1 receives lambda_{m+1}, or NULL
+    double *trace_U;               // [iters][B][R]: row m - 1 receives U_m, or NULL
 };
 
 constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
@@ -103,7 +122,8 @@ hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
-hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done,
-                          uint32_t *epoch, int32_t *status, int B, hipStream_t s);
+hipError_t launch_prepare(int R, const KArgs &a, const double *lam, int B, hipStream_t s);
+// Closing launch of a deferred solve: completes its last iteration (no selection).
+hipError_t launch_finish(int R, const KArgs &a, int B, hipStream_t s);
 
 }  // namespace esp

@@ -4,8 +4,14 @@
 //   score   s_jk = u_jk - sum_r lambda_r d_jkr          (Sec. 3.2.2, bracket of Eq. 6)
 //   select  c_j  = argmax_k s_jk, lowest k on ties     (Sec. 3.2.2 per-job subproblem)
 //   demand  U_r  = sum_j d_{j,c_j,r}, exact             (Sec. 3.2.3, under Eq. 8)
-//   update  lambda_r <- max(0, lambda_r + eta_t (U_r - C_r)) in the last
-//           workgroup of each cluster                   (Eq. 8)
+//   update  lambda_r <- max(0, lambda_r + eta_t (U_r - C_r))  (Eq. 8)
+//
+// With several workgroups per cluster, a solve iteration ends once every
+// workgroup has published its exact demand sums; every workgroup of the
+// cluster then computes U and the update itself at the start of the next
+// iteration (integer sums: all obtain the same bits), so no workgroup waits
+// for a last one to finish the update.  With one workgroup per cluster the
+// workgroup updates at the end of its own iteration.
 //
 // Table layout (built by the packer): per cluster, one fp32 column for the
 // utility and one per resource, each a sequence of 256-entry tiles.  A
@@ -31,9 +37,9 @@ namespace esp {
 // eta_t of Eq. 8 for the launch's step index t: eta0 or eta0 / sqrt(t), one
 // IEEE division and one correctly rounded square root in binary64 (no fast
 // math), so the value equals the host's.
-__device__ __forceinline__ double step_size(const KArgs &a, int cl) {
+__device__ __forceinline__ double step_size(const KArgs &a, int cl, int t) {
     const double e0 = a.eta0[cl];
-    return a.rule == 1 ? e0 / sqrt(static_cast<double>(a.t)) : e0;
+    return a.rule == 1 ? e0 / sqrt(static_cast<double>(t)) : e0;
 }
 
 // U_r from the cluster's exact total, the Eq. 8 update and the stop test for
@@ -49,10 +55,10 @@ __device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r,
     if (a.lam_out) {
         const double lo = a.lam_in[cl * R + r];
         const double g = U - a.cap[cl * R + r];
-        const double x = lo + step_size(a, cl) * g;
+        const double x = lo + step_size(a, cl, a.t) * g;
         const double ln = (x > 0.0) ? x : 0.0;
-        // agent-scope exchange: visible at the coherence point to the other
-        // workgroups of a persistent launch once it has returned
+        // agent-scope exchange: performed at the coherence point, where the
+        // next launch reads it
         const double prev = __hip_atomic_exchange(&a.lam_out[cl * R + r], ln, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
         asm volatile("s_waitcnt vmcnt(0)" : : "v"(prev) : "memory");
@@ -102,8 +108,155 @@ __device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum
 }
 
 // ---------------------------------------------------------------------------
-// Persistent launches: one launch runs n_iters iterations
+// Deferred completion (several workgroups per cluster)
 // ---------------------------------------------------------------------------
+
+// Complete iteration m of cluster cl (step index t_m) from the sums it
+// published into buffer m & 1, whose first loads (partial_loads) are in v:
+// U_m, lambda_{m+1} of Eq. 8 and the stop test.  lam_m (LDS) holds the
+// prices iteration m selected at; lam_next (LDS) receives lambda_{m+1};
+// s_red is LDS scratch.  All threads take part and get whether the tolerance
+// is met.  The writer (workgroup 0 of the cluster) also stores
+// lambda_{m+1} into the caller's prices and lam_ws, the trace rows of
+// iteration m, the iteration count, and m as the stop iteration.
+template <int R, typename A, bool Coherent>
+__device__ bool complete_iteration(const KArgs &a, int cl, int m, int t_m, bool writer, const double *lam_m,
+                                   double *lam_next, u128 *s_red, const A (&v)[kSumLoads]) {
+    __shared__ int s_ok[R];
+    partial_totals<R, A, Coherent>(a, m & 1, cl, v, s_red);
+    const int t = threadIdx.x;
+    if (t < R) {
+        const size_t i = static_cast<size_t>(cl) * R + t;
+        const double U = fx_to_double(s_red[t], a.shift[i]);
+        const double lo = lam_m[t];
+        const double g = U - a.cap[i];
+        const double x = lo + step_size(a, cl, t_m) * g;
+        const double ln = (x > 0.0) ? x : 0.0;
+        lam_next[t] = ln;
+        const double diff = fabs(ln - lo);
+        const double scale = lo > 1.0 ? lo : 1.0;
+        s_ok[t] = diff <= a.tol * scale;
+        if (writer) {
+            const size_t BR = static_cast<size_t>(a.B) * R;
+            a.lam_dst[i] = ln;
+            a.lam_ws[static_cast<size_t>((m + 1) & 1) * BR + i] = ln;
+            if (a.trace_U) a.trace_U[static_cast<size_t>(m - 1) * BR + i] = U;
+            if (a.trace_lam) a.trace_lam[static_cast<size_t>(m - 1) * BR + i] = ln;
+        }
+    }
+    __syncthreads();
+    int all = 1;
+#pragma unroll
+    for (int r = 0; r < R; ++r) all &= s_ok[r];
+    const bool stop = a.tol > 0.0 && all;
+    if (writer && t == 0) {
+        if (a.iters_done) a.iters_done[cl] = m;
+        if (stop) __hip_atomic_store(&a.conv_at[cl], m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return stop;
+}
+
+// The loads of a launch's pending completion (pend_m > 0).  They are issued
+// before the first tiles' loads, so they return first and the completion
+// runs while the tiles are still in flight; they are issued whether or not
+// the completion turns out to be needed.
+template <int R, typename A>
+struct Pending {
+    A v[kSumLoads];      // this thread's first published sums of iteration pend_m
+    double lam_m = 0.0;  // thread t < R: lambda_{pend_m}[t]
+    int conv = 0;        // conv_at[cl]
+};
+
+// conv: conv_at[cl], read by the caller at the start of the launch together
+// with the cluster's flags.  Within a launch conv_at changes only from 0 to
+// pend_m (workgroup 0 completing pend_m itself), and both values lead to the
+// same path, so a value read before that store is as good as one read after.
+// The loads are issued whether or not a completion is pending, from valid
+// addresses and without branches, so that the compiler waits for exactly
+// these loads (and not for the tile loads issued after them) where they are
+// used.
+template <int R, typename A>
+__device__ __forceinline__ void pending_loads(const KArgs &a, int cl, int conv, Pending<R, A> &p) {
+    const int k = a.pend_m & 1;
+    p.conv = conv;
+    p.lam_m = a.lam_ws[static_cast<size_t>(k) * a.B * R + static_cast<size_t>(cl) * R + threadIdx.x % R];
+    partial_loads<R, A, false>(a, k, cl, p.v);
+}
+
+// Prices of the launch's first iteration, into s_lam (LDS).  A launch with a
+// pending completion first completes iteration pend_m, unless the cluster
+// met the tolerance at an earlier iteration (conv_at 0 or pend_m: complete
+// it here; every workgroup then reaches the same decision).  Returns false
+// when the cluster has nothing left to do in this launch (it has converged
+// and the launch runs solve iterations).
+template <int R, typename A>
+__device__ bool launch_prices(const KArgs &a, int cl, int blk, const Pending<R, A> &p, double *s_lam,
+                              double *s_tmp, u128 *s_red) {
+    const int t = threadIdx.x;
+    if (a.pend_m > 0) {
+        if (p.conv == 0 || p.conv >= a.pend_m) {
+            if (t < R) s_tmp[t] = p.lam_m;
+            __syncthreads();
+            const bool stop =
+                complete_iteration<R, A, false>(a, cl, a.pend_m, a.pend_t, blk == 0, s_tmp, s_lam, s_red, p.v);
+            return !(stop && a.defer);
+        }
+        if (a.defer) return false;
+        // met the tolerance earlier: the caller's prices are final and are not
+        // written in this launch
+    }
+    if (t < R) s_lam[t] = a.lam_in[cl * R + t];
+    __syncthreads();
+    return true;
+}
+
+// End of iteration m in a deferred launch: publish the workgroup's sums
+// (bsum, LDS) into buffer m & 1.  A persistent launch publishes with
+// completed agent-scope exchanges and then counts one arrival in epoch[cl]
+// (reset by k_prepare), which reaches nblk * m once every workgroup has
+// published iteration m.  A one-iteration launch stores plainly: the next
+// launch reads the sums after the launch boundary.
+template <int R, bool Persist>
+__device__ __forceinline__ void publish_iteration(const KArgs &a, int cl, int blk, int m, const u128 *bsum) {
+    const int t = threadIdx.x;
+    if constexpr (Persist) {
+        if (t < kWaveSize) {
+            publish_sums<R>(a, m & 1, cl, blk, bsum);
+            if (t == 0) __hip_atomic_fetch_add(&a.epoch[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else if (t < R) {
+        uint64_t *p = partials_of<R>(a, m & 1, cl) + (static_cast<size_t>(blk) * R + t) * 2;
+        const u128 v = bsum[t];
+        p[0] = static_cast<uint64_t>(v);
+        p[1] = static_cast<uint64_t>(v >> 64);
+    }
+}
+
+// Inside a persistent launch: wait until every workgroup of the cluster has
+// published iteration m (epoch[cl] reaches nblk * m, compared modulo 2^32).
+// Bounded: about 2 s of the 100 MHz real-time counter, or until another
+// workgroup has recorded an error; then the status records a timeout and the
+// function returns false in every waiting workgroup.
+__device__ bool wait_iteration(const KArgs &a, int cl, int m, int *s_go) {
+    if (threadIdx.x == 0) {
+        const uint32_t target = static_cast<uint32_t>(a.nblk) * static_cast<uint32_t>(m);
+        int go = 1;
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        while (static_cast<int32_t>(__hip_atomic_load(&a.epoch[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
+                                    target) < 0) {
+            __builtin_amdgcn_s_sleep(2);
+            if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+                __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
+                atomicCAS(a.status, 0, kStatusTimeout);
+                go = 0;
+                break;
+            }
+        }
+        *s_go = go;
+    }
+    __syncthreads();
+    return *s_go != 0;
+}
 
 // Per-iteration view of the arguments of a persistent launch.
 template <int R>
@@ -119,53 +272,14 @@ __device__ __forceinline__ KArgs iteration_args(const KArgs &a, int it) {
     return ai;
 }
 
-// After iteration `it` of a persistent launch: thread 0 of the last
-// workgroup has published the new prices (atomic exchanges) and reset the
-// ticket; it now bumps the cluster's epoch.  Every workgroup then waits for
-// the epoch (bounded: a timeout records an error and ends the launch) and
-// reads the new prices and the stop flag with agent-scope atomic loads.
-// Returns false when the workgroup must leave the iteration loop.
+// Between the iterations of a persistent launch with one workgroup per
+// cluster: the workgroup computed the new prices itself (s_newlam) and
+// continues with them unless the cluster has stopped.
 template <int R>
-__device__ bool persist_barrier(const KArgs &a, int cl, int it, bool was_last, double *s_lam, int *s_go,
-                                const double *s_newlam, const int *s_stop) {
-    const int t = threadIdx.x;
-    if (a.nblk == 1) {
-        // The only workgroup of the cluster computed the prices itself.
-        __syncthreads();
-        if (*s_stop) return false;
-        if (t < R) s_lam[t] = s_newlam[t];
-        __syncthreads();
-        return true;
-    }
-    const uint32_t target = a.epoch_base + static_cast<uint32_t>(it) + 1u;
-    if (t == 0) {
-        if (was_last) {
-            asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // flag updates complete
-            __hip_atomic_fetch_add(&a.epoch[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        int go = 1;
-        // Bounded wait: about 2 s of the 100 MHz real-time counter, or until
-        // another workgroup has recorded an error.
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        while (__hip_atomic_load(&a.epoch[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            __builtin_amdgcn_s_sleep(2);
-            if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
-                __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
-                atomicCAS(a.status, 0, kStatusTimeout);
-                go = 0;
-                break;
-            }
-        }
-        if (go && a.flags &&
-            (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & (kFlagStopped | kFlagError)))
-            go = 0;
-        *s_go = go;
-    }
+__device__ __forceinline__ bool next_prices_local(double *s_lam, const double *s_newlam, const int *s_stop) {
     __syncthreads();
-    if (!*s_go) return false;
-    if (t < R)
-        s_lam[t] = __hip_atomic_load(const_cast<double *>(&a.lam_in[cl * R + t]), __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
+    if (*s_stop) return false;
+    if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
     __syncthreads();
     return true;
 }
@@ -174,7 +288,14 @@ __device__ bool persist_barrier(const KArgs &a, int cl, int it, bool was_last, d
 // Dense families: K = 4 * LPJ configurations per job, LPJ lanes per job
 // ---------------------------------------------------------------------------
 
-template <int R, int LPJ, typename A>
+// Launch modes of the fused kernels, one instance each, so that the
+// one-iteration instance does without the code (and the registers) of the
+// multi-iteration ones.
+constexpr int kOnePass = 0;          // one iteration or one selection per launch
+constexpr int kPersistLocal = 1;     // cooperative, several iterations, one workgroup per cluster
+constexpr int kPersistDeferred = 2;  // cooperative, several iterations, deferred completion between them
+
+template <int R, int LPJ, typename A, int Mode>
 __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     constexpr int JPT = kWaveSize / LPJ;       // jobs per tile
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
@@ -189,14 +310,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
 
     const int cl = blockIdx.x / a.nblk;
     const int blk = blockIdx.x - cl * a.nblk;
+    const int conv = a.conv_at[cl];            // with the flags: one wait for both
     if (a.flags && (a.flags[cl] & a.skip_mask)) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (threadIdx.x == 0) s_stop = 0;
 
-    double lam[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) lam[r] = a.lam_in[cl * R + r];
+    double lam[R];                             // prices of the current iteration
 
     const float *col = a.table + cl * a.cluster_stride;
     const int my_r = lane % R;
@@ -273,21 +393,32 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     f4 ua, ub, uc, pa = {}, pb = {}, pc = {};
     f4 da[R], db[R], dc[R];
     const int tile0 = blk * kBlockWaves + wave;
+    // Loads of tiles past the end are clamped to the last tile (never
+    // processed): no branches, so that the compiler's waits for earlier loads
+    // do not wait for these.
     auto prefetch_two = [&](int rev) {
-        if (tile0 < a.tiles) load_tile(tile0, rev, ua, da, pa);
-        if (tile0 + stride < a.tiles) load_tile(tile0 + stride, rev, ub, db, pb);
+        load_tile(min(tile0, last), rev, ua, da, pa);
+        load_tile(min(tile0 + stride, last), rev, ub, db, pb);
     };
-    prefetch_two(a.reverse);
+    Pending<R, A> pend;
+    pending_loads<R, A>(a, cl, conv, pend);    // issued first: they return first
+    prefetch_two(a.reverse);                   // in flight during a pending completion
+    if (!launch_prices<R, A>(a, cl, blk, pend, s_lam, s_newlam, s_acc)) return;
+#pragma unroll
+    for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     for (int it = 0; it < a.n_iters; ++it) {
         const KArgs ai = iteration_args<R>(a, it);
         const int rev = ai.reverse;
+        // Loads past the end are clamped to the last tile (never processed):
+        // without branches around them the compiler waits for each tile's
+        // own loads only.
         for (int tile = tile0; tile < a.tiles; tile += 3 * stride) {
             const int t1 = tile + stride, t2 = tile + 2 * stride;
-            if (t2 < a.tiles) load_tile(t2, rev, uc, dc, pc);
+            load_tile(min(t2, last), rev, uc, dc, pc);
             process(ai, tile, ua, da, pa);
-            if (t2 + stride < a.tiles) load_tile(t2 + stride, rev, ua, da, pa);
+            load_tile(min(t2 + stride, last), rev, ua, da, pa);
             if (t1 < a.tiles) process(ai, t1, ub, db, pb);
-            if (t2 + 2 * stride < a.tiles) load_tile(t2 + 2 * stride, rev, ub, db, pb);
+            load_tile(min(t2 + 2 * stride, last), rev, ub, db, pb);
             if (t2 < a.tiles) process(ai, t2, uc, dc, pc);
         }
         if (!ai.reduce) return;
@@ -311,10 +442,22 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             s_bsum[threadIdx.x] = v;
         }
         __syncthreads();
-        const bool was_last = finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
-        if (it + 1 == a.n_iters) break;
-        prefetch_two(rev ^ a.sweep_alt);
-        if (!persist_barrier<R>(a, cl, it, was_last, s_lam, &s_go, s_newlam, &s_stop)) break;
+        if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
+            publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
+            if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
+            prefetch_two(rev ^ a.sweep_alt);
+            if (!wait_iteration(a, cl, ai.iter_no, &s_go)) break;
+            A v[kSumLoads];
+            partial_loads<R, A, true>(ai, ai.iter_no & 1, cl, v);
+            if (complete_iteration<R, A, true>(ai, cl, ai.iter_no, ai.t, blk == 0, s_lam, s_newlam, s_acc, v)) break;
+            if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
+            __syncthreads();
+        } else {
+            finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+            if (Mode == kOnePass || it + 1 == a.n_iters) break;
+            prefetch_two(rev ^ a.sweep_alt);
+            if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
+        }
 #pragma unroll
         for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     }
@@ -363,7 +506,7 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
     }
 }
 
-template <int R, typename A>
+template <int R, typename A, int Mode>
 __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
     __shared__ uint32_t s_win[kBlockWaves][8];
@@ -378,14 +521,13 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
 
     const int cl = blockIdx.x / a.nblk;
     const int blk = blockIdx.x - cl * a.nblk;
+    const int conv = a.conv_at[cl];            // with the flags: one wait for both
     if (a.flags && (a.flags[cl] & a.skip_mask)) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (threadIdx.x == 0) s_stop = 0;
 
-    double lam[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) lam[r] = a.lam_in[cl * R + r];
+    double lam[R];                             // prices of the current iteration
     const int my_r = lane % R;
     const int my_q = lane / R;
     const bool acc_lane = lane < Q * R;
@@ -531,7 +673,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     f4 nd[R];
     uint32_t nhw = 0;
     const int tile0 = blk * kBlockWaves + wave;
-    if (tile0 < a.tiles) load_tile(tile0, a.reverse, nu, nd, npn, nhw);
+    Pending<R, A> pend;
+    pending_loads<R, A>(a, cl, conv, pend);    // issued first: they return first
+    load_tile(min(tile0, last), a.reverse, nu, nd, npn, nhw);   // in flight during a pending completion (clamped: no branch)
+    if (!launch_prices<R, A>(a, cl, blk, pend, s_lam, s_newlam, s_acc)) return;
+#pragma unroll
+    for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     for (int it = 0; it < a.n_iters; ++it) {
         const KArgs ai = iteration_args<R>(a, it);
         const int rev = ai.reverse;
@@ -541,7 +688,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
 #pragma unroll
             for (int r = 0; r < R; ++r) d[r] = nd[r];
             const uint32_t hw = nhw;
-            if (tile + stride < a.tiles) load_tile(tile + stride, rev, nu, nd, npn, nhw);
+            load_tile(min(tile + stride, last), rev, nu, nd, npn, nhw);   // clamped: no branch
             process(ai, tile, u, d, pn, hw);
         }
         if (!ai.reduce) return;
@@ -564,10 +711,22 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             s_bsum[threadIdx.x] = v;
         }
         __syncthreads();
-        const bool was_last = finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
-        if (it + 1 == a.n_iters) break;
-        if (tile0 < a.tiles) load_tile(tile0, rev ^ a.sweep_alt, nu, nd, npn, nhw);
-        if (!persist_barrier<R>(a, cl, it, was_last, s_lam, &s_go, s_newlam, &s_stop)) break;
+        if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
+            publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
+            if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
+            load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
+            if (!wait_iteration(a, cl, ai.iter_no, &s_go)) break;
+            A v[kSumLoads];
+            partial_loads<R, A, true>(ai, ai.iter_no & 1, cl, v);
+            if (complete_iteration<R, A, true>(ai, cl, ai.iter_no, ai.t, blk == 0, s_lam, s_newlam, s_acc, v)) break;
+            if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
+            __syncthreads();
+        } else {
+            finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+            if (Mode == kOnePass || it + 1 == a.n_iters) break;
+            load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
+            if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
+        }
 #pragma unroll
         for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
     }
@@ -655,23 +814,42 @@ __global__ void k_update(KArgs a, const double *demand_in, int B) {
     for (int r = 0; r < R; ++r) {
         const double lo = a.lam_in[cl * R + r];
         const double g = demand_in[cl * R + r] - a.cap[cl * R + r];
-        const double x = lo + step_size(a, cl) * g;
+        const double x = lo + step_size(a, cl, a.t) * g;
         a.lam_out[cl * R + r] = (x > 0.0) ? x : 0.0;
     }
 }
 
-// Validate prices before a solve or a selection; mark bad clusters.
+// Validate prices before a solve or a selection; mark bad clusters.  For a
+// solve (iters_done set) also reset the per-solve counters and store the
+// starting prices as lambda_1 (lam_ws[1]) for the first deferred completion.
 template <int R>
-__global__ void k_prepare(const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch, int32_t *status,
-                          int B) {
+__global__ void k_prepare(KArgs a, const double *lam, int B) {
     const int cl = blockIdx.x * blockDim.x + threadIdx.x;
     if (cl >= B) return;
     bool ok = true;
     for (int r = 0; r < R; ++r) ok = ok && price_ok(lam[cl * R + r]);
-    flags[cl] = (flags[cl] & kFlagFrozen) | (ok ? 0 : kFlagError);
-    if (iters_done) iters_done[cl] = 0;
-    if (epoch) epoch[cl] = 0u;
-    if (!ok) atomicCAS(status, 0, kStatusNonfinite);
+    a.flags[cl] = (a.flags[cl] & kFlagFrozen) | (ok ? 0 : kFlagError);
+    if (a.iters_done) {
+        a.iters_done[cl] = 0;
+        a.epoch[cl] = 0u;
+        a.conv_at[cl] = 0;
+        for (int r = 0; r < R; ++r) a.lam_ws[static_cast<size_t>(B) * R + static_cast<size_t>(cl) * R + r] = lam[cl * R + r];
+    }
+    if (!ok) atomicCAS(a.status, 0, kStatusNonfinite);
+}
+
+// Closing launch of a deferred solve without a final selection: one
+// workgroup per cluster completes the solve's last iteration (pend_m).
+template <int R>
+__global__ __launch_bounds__(kBlockThreads) void k_finish(KArgs a) {
+    __shared__ u128 s_red[kBlockThreads];
+    __shared__ double s_tmp[R];
+    __shared__ double s_lam[R];
+    const int cl = blockIdx.x;
+    if (a.flags && (a.flags[cl] & a.skip_mask)) return;
+    Pending<R, u128> pend;
+    pending_loads<R, u128>(a, cl, a.conv_at[cl], pend);
+    (void)launch_prices<R, u128>(a, cl, 0, pend, s_lam, s_tmp, s_red);
 }
 
 // ---------------------------------------------------------------------------
@@ -682,11 +860,11 @@ template <int R, typename A>
 static hipError_t launch_dense_ra(int lpj, const KArgs &a, int B, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
     switch (lpj) {
-        case 1: hipLaunchKernelGGL((k_dense<R, 1, A>), grid, block, 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_dense<R, 2, A>), grid, block, 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_dense<R, 4, A>), grid, block, 0, s, a); break;
-        case 8: hipLaunchKernelGGL((k_dense<R, 8, A>), grid, block, 0, s, a); break;
-        case 16: hipLaunchKernelGGL((k_dense<R, 16, A>), grid, block, 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_dense<R, 1, A, kOnePass>), grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_dense<R, 2, A, kOnePass>), grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_dense<R, 4, A, kOnePass>), grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL((k_dense<R, 8, A, kOnePass>), grid, block, 0, s, a); break;
+        case 16: hipLaunchKernelGGL((k_dense<R, 16, A, kOnePass>), grid, block, 0, s, a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -701,11 +879,16 @@ template <int R, typename A>
 static hipError_t launch_dense_coop_ra(int lpj, const KArgs &a, int B, hipStream_t s) {
     const void *f = nullptr;
     switch (lpj) {
-        case 1: f = reinterpret_cast<const void *>(&k_dense<R, 1, A>); break;
-        case 2: f = reinterpret_cast<const void *>(&k_dense<R, 2, A>); break;
-        case 4: f = reinterpret_cast<const void *>(&k_dense<R, 4, A>); break;
-        case 8: f = reinterpret_cast<const void *>(&k_dense<R, 8, A>); break;
-        case 16: f = reinterpret_cast<const void *>(&k_dense<R, 16, A>); break;
+        case 1: f = a.defer ? reinterpret_cast<const void *>(&k_dense<R, 1, A, kPersistDeferred>)
+                           : reinterpret_cast<const void *>(&k_dense<R, 1, A, kPersistLocal>); break;
+        case 2: f = a.defer ? reinterpret_cast<const void *>(&k_dense<R, 2, A, kPersistDeferred>)
+                           : reinterpret_cast<const void *>(&k_dense<R, 2, A, kPersistLocal>); break;
+        case 4: f = a.defer ? reinterpret_cast<const void *>(&k_dense<R, 4, A, kPersistDeferred>)
+                           : reinterpret_cast<const void *>(&k_dense<R, 4, A, kPersistLocal>); break;
+        case 8: f = a.defer ? reinterpret_cast<const void *>(&k_dense<R, 8, A, kPersistDeferred>)
+                           : reinterpret_cast<const void *>(&k_dense<R, 8, A, kPersistLocal>); break;
+        case 16: f = a.defer ? reinterpret_cast<const void *>(&k_dense<R, 16, A, kPersistDeferred>)
+                           : reinterpret_cast<const void *>(&k_dense<R, 16, A, kPersistLocal>); break;
         default: return hipErrorInvalidValue;
     }
     KArgs copy = a;
@@ -715,6 +898,7 @@ static hipError_t launch_dense_coop_ra(int lpj, const KArgs &a, int B, hipStream
 
 template <int R>
 static hipError_t launch_dense_coop_r(int lpj, const KArgs &a, int B, hipStream_t s) {
+    if (!a.defer && a.nblk != 1) return hipErrorInvalidValue;   // several workgroups need deferred completion
     return a.acc128 ? launch_dense_coop_ra<R, u128>(lpj, a, B, s) : launch_dense_coop_ra<R, uint64_t>(lpj, a, B, s);
 }
 
@@ -759,16 +943,25 @@ hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, 
 }
 
 template <int R>
-static hipError_t launch_prepare_r(const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch,
-                                   int32_t *status, int B, hipStream_t s) {
-    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, lam, flags, iters_done, epoch, status,
-                       B);
+static hipError_t launch_prepare_r(const KArgs &a, const double *lam, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, a, lam, B);
     return hipGetLastError();
 }
 
-hipError_t launch_prepare(int R, const double *lam, int32_t *flags, int32_t *iters_done, uint32_t *epoch,
-                          int32_t *status, int B, hipStream_t s) {
-#define CALL(RR) launch_prepare_r<RR>(lam, flags, iters_done, epoch, status, B, s)
+hipError_t launch_prepare(int R, const KArgs &a, const double *lam, int B, hipStream_t s) {
+#define CALL(RR) launch_prepare_r<RR>(a, lam, B, s)
+    ESP_DISPATCH_R(R, CALL)
+#undef CALL
+}
+
+template <int R>
+static hipError_t launch_finish_r(const KArgs &a, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_finish<R>), dim3(static_cast<unsigned>(B)), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_finish(int R, const KArgs &a, int B, hipStream_t s) {
+#define CALL(RR) launch_finish_r<RR>(a, B, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }
@@ -777,16 +970,19 @@ template <int R>
 static hipError_t launch_csr_r(const KArgs &a, int B, hipStream_t s) {
     const dim3 grid(static_cast<unsigned>(B) * a.nblk), block(kBlockThreads);
     if (a.acc128)
-        hipLaunchKernelGGL((k_csr<R, u128>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_csr<R, u128, kOnePass>), grid, block, 0, s, a);
     else
-        hipLaunchKernelGGL((k_csr<R, uint64_t>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_csr<R, uint64_t, kOnePass>), grid, block, 0, s, a);
     return hipGetLastError();
 }
 
 template <int R>
 static hipError_t launch_csr_coop_r(const KArgs &a, int B, hipStream_t s) {
-    const void *f = a.acc128 ? reinterpret_cast<const void *>(&k_csr<R, u128>)
-                             : reinterpret_cast<const void *>(&k_csr<R, uint64_t>);
+    if (!a.defer && a.nblk != 1) return hipErrorInvalidValue;   // several workgroups need deferred completion
+    const void *f = a.acc128 ? (a.defer ? reinterpret_cast<const void *>(&k_csr<R, u128, kPersistDeferred>)
+                                        : reinterpret_cast<const void *>(&k_csr<R, u128, kPersistLocal>))
+                             : (a.defer ? reinterpret_cast<const void *>(&k_csr<R, uint64_t, kPersistDeferred>)
+                                        : reinterpret_cast<const void *>(&k_csr<R, uint64_t, kPersistLocal>));
     KArgs copy = a;
     void *args[] = {&copy};
     return hipLaunchCooperativeKernel(f, dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), args, 0, s);
