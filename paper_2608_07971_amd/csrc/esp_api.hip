@@ -41,7 +41,7 @@ struct Plan {
     int aos_stride = 0; // floats per entry of the entry-major copy, 0 when there is none
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
-           o_tick = 0, o_flags = 0, o_iters = 0, o_epoch = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
+           o_tick = 0, o_flags = 0, o_iters = 0, o_sync = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
            o_aos = 0, o_lamws = 0, o_conv = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
@@ -159,7 +159,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_tick = o;  o = align_up(o + B * sizeof(uint32_t));
     pl->o_flags = o; o = align_up(o + B * sizeof(int32_t));
     pl->o_iters = o; o = align_up(o + B * sizeof(int32_t));
-    pl->o_epoch = o; o = align_up(o + B * sizeof(uint32_t));
+    pl->o_sync = o;  o = align_up(o + B * kSyncSlots * kSyncStride * sizeof(uint32_t));
     pl->o_swc = o;   o = align_up(o + B * sizeof(double));
     pl->o_status = o; o = align_up(o + sizeof(int32_t));
     pl->o_capp = o;  o = align_up(o + B * R * sizeof(double));
@@ -537,7 +537,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemsetAsync(ws + pl.o_tick, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_flags, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_iters, 0, sizeof(int32_t) * B, s) == hipSuccess &&
-                  hipMemsetAsync(ws + pl.o_epoch, 0, sizeof(uint32_t) * B, s) == hipSuccess &&
+                  hipMemsetAsync(ws + pl.o_sync, 0, sizeof(uint32_t) * B * kSyncSlots * kSyncStride, s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_conv, 0, sizeof(int32_t) * B, s) == hipSuccess &&
                   hipMemcpyAsync(ws + pl.o_swc, swc.data(), sizeof(double) * B, hipMemcpyHostToDevice, s) ==
                       hipSuccess &&
@@ -581,7 +581,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.acc128 = need_bits > 63 ? 1 : 0;
     k.n_iters = 1;
     k.B = B;
-    k.epoch = reinterpret_cast<uint32_t *>(ws + pl.o_epoch);
+    k.sync = reinterpret_cast<uint32_t *>(ws + pl.o_sync);
     k.lam_ws = reinterpret_cast<double *>(ws + pl.o_lamws);
     k.conv_at = reinterpret_cast<int32_t *>(ws + pl.o_conv);
     k.sweep_alt = c->sweep == 0 ? 1 : 0;

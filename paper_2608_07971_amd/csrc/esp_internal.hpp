@@ -18,6 +18,12 @@ constexpr int kMaxR = 8;
 constexpr int kMaxFamily = 256;                     // configurations per job
 constexpr int kLaunchChunk = 1024;                  // iterations per persistent launch
 constexpr int kColumnPadTiles = 7;                  // unused tiles at the end of every column
+// Barrier words of a cluster in a persistent deferred launch, each in its own
+// 256-byte line: arrival counters of kSyncGroups groups of workgroups (blk mod
+// kSyncGroups), the count of complete groups, and one release word per group.
+constexpr int kSyncGroups = 8;
+constexpr int kSyncSlots = 2 * kSyncGroups + 1;
+constexpr int kSyncStride = 64;                     // uint32 words between barrier words
 // Buffers of per-workgroup sums: 0 and 1 hold the sums of solve iterations by
 // iteration parity (deferred completion), 2 those of in-launch completion.
 constexpr int kPartialBuffers = 3;
@@ -88,7 +94,8 @@ struct KArgs {
     // sweep direction alternates.
     int32_t n_iters;               // 1 for a single-iteration launch
     int32_t B;                     // clusters
-    uint32_t *epoch;               // [B] workgroup arrivals of deferred iterations (reset per solve)
+    uint32_t *sync;                // [B][kSyncSlots][kSyncStride] barrier words of persistent
+                                   // deferred launches (reset per solve)
     int32_t sweep_alt;             // alternate the sweep direction between iterations
     // Penalty of the ESP score (Eq. 7): column R + 1 of each cluster holds
     // |penalty| per entry, its sign bit set when the entry is not the job's

@@ -210,19 +210,43 @@ __device__ bool launch_prices(const KArgs &a, int cl, int blk, const Pending<R, 
     return true;
 }
 
+// Barrier word i of cluster cl (see kSyncSlots).
+__device__ __forceinline__ uint32_t *sync_word(const KArgs &a, int cl, int i) {
+    return a.sync + (static_cast<size_t>(cl) * kSyncSlots + i) * kSyncStride;
+}
+
 // End of iteration m in a deferred launch: publish the workgroup's sums
-// (bsum, LDS) into buffer m & 1.  A persistent launch publishes with
-// completed agent-scope exchanges and then counts one arrival in epoch[cl]
-// (reset by k_prepare), which reaches nblk * m once every workgroup has
-// published iteration m.  A one-iteration launch stores plainly: the next
-// launch reads the sums after the launch boundary.
+// (bsum, LDS) into buffer m & 1.  A one-iteration launch stores plainly: the
+// next launch reads the sums after the launch boundary.  A persistent launch
+// publishes with completed agent-scope exchanges and then arrives at the
+// cluster's barrier: one atomic add on its group's counter (blk mod
+// kSyncGroups); the group's last arrival adds one to the count of complete
+// groups, and the last group's releases every group by storing m into the
+// groups' release words.  Adds to one address are serialized at the device
+// coherence point (about 11 ns each), so no word takes more than one add per
+// group member per iteration, and each group polls its own release word.
 template <int R, bool Persist>
 __device__ __forceinline__ void publish_iteration(const KArgs &a, int cl, int blk, int m, const u128 *bsum) {
     const int t = threadIdx.x;
     if constexpr (Persist) {
         if (t < kWaveSize) {
             publish_sums<R>(a, m & 1, cl, blk, bsum);
-            if (t == 0) __hip_atomic_fetch_add(&a.epoch[cl], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (t == 0) {
+                const int g = blk % kSyncGroups;
+                const int groups = a.nblk < kSyncGroups ? a.nblk : kSyncGroups;
+                const uint32_t size = static_cast<uint32_t>((a.nblk - g + kSyncGroups - 1) / kSyncGroups);
+                const uint32_t um = static_cast<uint32_t>(m);
+                const uint32_t n = __hip_atomic_fetch_add(sync_word(a, cl, g), 1u, __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT);
+                if (n + 1u == size * um) {
+                    const uint32_t c = __hip_atomic_fetch_add(sync_word(a, cl, kSyncGroups), 1u, __ATOMIC_RELAXED,
+                                                              __HIP_MEMORY_SCOPE_AGENT);
+                    if (c + 1u == static_cast<uint32_t>(groups) * um)
+                        for (int h = 0; h < groups; ++h)
+                            __hip_atomic_store(sync_word(a, cl, kSyncGroups + 1 + h), um, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
         }
     } else if (t < R) {
         uint64_t *p = partials_of<R>(a, m & 1, cl) + (static_cast<size_t>(blk) * R + t) * 2;
@@ -232,19 +256,20 @@ __device__ __forceinline__ void publish_iteration(const KArgs &a, int cl, int bl
     }
 }
 
-// Inside a persistent launch: wait until every workgroup of the cluster has
-// published iteration m (epoch[cl] reaches nblk * m, compared modulo 2^32).
-// Bounded: about 2 s of the 100 MHz real-time counter, or until another
-// workgroup has recorded an error; then the status records a timeout and the
-// function returns false in every waiting workgroup.
-__device__ bool wait_iteration(const KArgs &a, int cl, int m, int *s_go) {
+// Inside a persistent launch: wait until the workgroup's group is released
+// for iteration m (its release word reaches m, compared modulo 2^32), i.e.
+// every workgroup of the cluster has published iteration m.  Bounded: about
+// 2 s of the 100 MHz real-time counter, or until another workgroup has
+// recorded an error; then the status records a timeout and the function
+// returns false in every waiting workgroup.
+__device__ bool wait_iteration(const KArgs &a, int cl, int blk, int m, int *s_go) {
     if (threadIdx.x == 0) {
-        const uint32_t target = static_cast<uint32_t>(a.nblk) * static_cast<uint32_t>(m);
+        const uint32_t *w = sync_word(a, cl, kSyncGroups + 1 + blk % kSyncGroups);
         int go = 1;
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        while (static_cast<int32_t>(__hip_atomic_load(&a.epoch[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
-                                    target) < 0) {
-            __builtin_amdgcn_s_sleep(2);
+        while (static_cast<int32_t>(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) -
+                                    static_cast<uint32_t>(m)) < 0) {
+            __builtin_amdgcn_s_sleep(4);
             if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
                 __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
                 atomicCAS(a.status, 0, kStatusTimeout);
@@ -446,7 +471,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
             prefetch_two(rev ^ a.sweep_alt);
-            if (!wait_iteration(a, cl, ai.iter_no, &s_go)) break;
+            if (!wait_iteration(a, cl, blk, ai.iter_no, &s_go)) break;
             A v[kSumLoads];
             partial_loads<R, A, true>(ai, ai.iter_no & 1, cl, v);
             if (complete_iteration<R, A, true>(ai, cl, ai.iter_no, ai.t, blk == 0, s_lam, s_newlam, s_acc, v)) break;
@@ -715,7 +740,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
             load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
-            if (!wait_iteration(a, cl, ai.iter_no, &s_go)) break;
+            if (!wait_iteration(a, cl, blk, ai.iter_no, &s_go)) break;
             A v[kSumLoads];
             partial_loads<R, A, true>(ai, ai.iter_no & 1, cl, v);
             if (complete_iteration<R, A, true>(ai, cl, ai.iter_no, ai.t, blk == 0, s_lam, s_newlam, s_acc, v)) break;
@@ -831,7 +856,7 @@ __global__ void k_prepare(KArgs a, const double *lam, int B) {
     a.flags[cl] = (a.flags[cl] & kFlagFrozen) | (ok ? 0 : kFlagError);
     if (a.iters_done) {
         a.iters_done[cl] = 0;
-        a.epoch[cl] = 0u;
+        for (int i = 0; i < kSyncSlots; ++i) a.sync[(static_cast<size_t>(cl) * kSyncSlots + i) * kSyncStride] = 0u;
         a.conv_at[cl] = 0;
         for (int r = 0; r < R; ++r) a.lam_ws[static_cast<size_t>(B) * R + static_cast<size_t>(cl) * R + r] = lam[cl * R + r];
     }
