@@ -68,13 +68,13 @@ enum {
                                  ESP_AUTO_PERSISTENT_BYTES), where launch latency would dominate,
                                  and for solves with tol > 0 (the loop ends on the device once
                                  every cluster has converged); one launch per iteration
-                                 otherwise, where the two drivers run at the same speed; falls
+                                 otherwise, where the two drivers run at about the same speed; falls
                                  back to one launch per iteration when the device cannot hold
                                  the grid co-resident */
     ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
-    ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; workgroups meet at a
-                                 per-cluster epoch after each price update (ESP_ERR_DEVICE when the
-                                 grid cannot be co-resident) */
+    ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; the workgroups of a
+                                 cluster meet at a barrier after each iteration (ESP_ERR_DEVICE
+                                 when the grid cannot be co-resident) */
 };
 
 #define ESP_AUTO_PERSISTENT_BYTES (64u << 20)
@@ -191,10 +191,11 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
 
 /*
  * esp_solve: `iters` iterations t = t_start .. t_start+iters-1 of
- * select -> demand -> update, one fused kernel pass per iteration (the update
- * runs in the last workgroup of each cluster; the passes run as one launch
- * each or inside one persistent launch, see ESP_MODE_*), then a re-selection
- * at the final prices (Alg. 1).
+ * select -> demand -> update, one fused kernel pass per iteration (the passes
+ * run as one launch each or inside one persistent launch, see ESP_MODE_*;
+ * with several workgroups per cluster the update of iteration t is computed
+ * at the start of the next pass, or of a closing launch after the last one),
+ * then a re-selection at the final prices (Alg. 1).
  *   prices      device [B][R], in lambda^{t_start} (finite, >= 0), out the final prices
  *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
  * Graph capture: while `stream` is being captured, the iterations are
