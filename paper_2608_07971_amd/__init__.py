@@ -329,13 +329,14 @@ class Solver:
         esp_update_prices(self.ctx, demand, t, prices, stream)
 
     def solve(self, prices: torch.Tensor, iters: int, t_start: int = 1, tol: float = 0.0, trace: bool = False,
-              trace_choice: bool = False, stream=None) -> dict:
-        """Run `iters` iterations in place on `prices`; returns device tensors."""
-        out = {
-            "choice": torch.empty((self.B, self.N), dtype=torch.int32, device=self.device),
-            "U": torch.empty((self.B, self.R), dtype=torch.float64, device=self.device),
-            "iters_done": torch.empty(self.B, dtype=torch.int32, device=self.device),
-        }
+              trace_choice: bool = False, stream=None, final_select: bool = True) -> dict:
+        """Run `iters` iterations in place on `prices`; returns device tensors.
+        final_select=False omits the re-selection at the final prices (no
+        "choice" / "U" outputs)."""
+        out = {"iters_done": torch.empty(self.B, dtype=torch.int32, device=self.device)}
+        if final_select:
+            out["choice"] = torch.empty((self.B, self.N), dtype=torch.int32, device=self.device)
+            out["U"] = torch.empty((self.B, self.R), dtype=torch.float64, device=self.device)
         tr = None
         if trace or trace_choice:
             T = max(int(iters), 1)
@@ -346,7 +347,8 @@ class Solver:
             if trace_choice:
                 out["tr_choice"] = torch.full((T, self.B, self.N), -1, dtype=torch.int32, device=self.device)
             tr = esp_trace(_ptr(out.get("tr_lam")), _ptr(out.get("tr_U")), _ptr(out.get("tr_choice")))
-        esp_solve(self.ctx, prices, iters, t_start, tol, out["choice"], out["U"], tr, out["iters_done"], stream)
+        esp_solve(self.ctx, prices, iters, t_start, tol, out.get("choice"), out.get("U"), tr, out["iters_done"],
+                  stream)
         out["lam"] = prices
         return out
 
