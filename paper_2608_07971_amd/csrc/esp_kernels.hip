@@ -221,7 +221,7 @@ __device__ __forceinline__ uint32_t *sync_word(const KArgs &a, int cl, int i) {
 // publishes with completed agent-scope exchanges and then arrives at the
 // cluster's barrier: one atomic add on its group's counter (blk mod
 // kSyncGroups); the group's last arrival adds one to the count of complete
-// groups, and the last group's releases every group by storing m into the
+// groups, and the last group releases every group by storing m into the
 // groups' release words.  Adds to one address are serialized at the device
 // coherence point (about 11 ns each), so no word takes more than one add per
 // group member per iteration, and each group polls its own release word.
