@@ -39,6 +39,9 @@ def _parse():
     ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
     ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
     ap.add_argument("--mode", type=int, default=0, help="loop driver: 0 auto, 1 one launch per iteration, 2 persistent")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step (price reset + esp_solve, one launch per pass) in a HIP graph and time "
+                         "its replays")
     ap.add_argument("--penalties", action="store_true",
                     help="add Eq. 7 penalty inputs (current configurations, switching cost, interference penalty)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the CPU-baseline sample")
@@ -90,7 +93,22 @@ def _cpu_baseline(inst, budget_s: float) -> dict:
         "sample": f"{inst.name}: first {n} price iterations of cluster 0 from lambda^1 = 0 "
                   f"({el:.1f} s, single-threaded C oracle, fp64)",
         "iters_per_s": 1.0 / per_iter,
+        "host": _host_cpu(),
     }
+
+
+def _host_cpu() -> str:
+    """CPU model and logical CPU count of the host the baseline ran on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{model}, {os.cpu_count()} logical CPUs (the baseline uses one thread)"
 
 
 def main() -> int:
@@ -140,26 +158,36 @@ def main() -> int:
         lam.copy_(lam0)
         solver.solve(lam, T, stream=stream)
 
+    run = step
+    if args.graph:
+        # static output buffers, one captured step; replays rerun it on them
+        graph = torch.cuda.CUDAGraph()
+        choice = torch.empty((solver.B, solver.N), dtype=torch.int32, device="cuda:0")
+        demand = torch.empty((solver.B, solver.R), dtype=torch.float64, device="cuda:0")
+        with torch.cuda.graph(graph, stream=stream):
+            lam.copy_(lam0)
+            esp.esp_solve(solver.ctx, lam, T, 1, 0.0, choice, demand, None, None, torch.cuda.current_stream())
+        run = graph.replay
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
-            step()
+            run()
     torch.cuda.synchronize()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
-        ev0.record(stream)
-        for _ in range(args.steps):
-            step()
-        ev1.record(stream)
+        evs[0].record(stream)
+        for i in range(args.steps):
+            run()
+            evs[i + 1].record(stream)
     torch.cuda.synchronize()
-    ms_total = ev0.elapsed_time(ev1)
+    ms_total = evs[0].elapsed_time(evs[-1])
+    step_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
     assert solver.device_status() == 0
     ms_per_step = ms_total / args.steps
     sec = ms_total / 1e3
     configs = inst.B * inst.nnz
     passes = (T + 1) * args.steps                    # T fused iterations + the final re-selection
-    persistent = solver.loop_driver() == esp.ESP_MODE_PERSISTENT
+    persistent = solver.loop_driver() == esp.ESP_MODE_PERSISTENT and not args.graph
     # algorithmic bytes: the fp32 table read once per iteration, plus the
     # family boundaries (one 4-byte offset per job) for ragged families
     csr = inst.dense_k is None or inst.dense_k not in (4, 8, 16, 32, 64)
@@ -183,6 +211,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "step_ms": {"min": step_ms[0], "median": step_ms[len(step_ms) // 2], "max": step_ms[-1]},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -197,7 +226,8 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": ("k_csr" if csr else "k_dense") + " (fused score/select/demand/update)",
-                     "driver": ("persistent: one cooperative launch runs the T passes" if persistent
+                     "driver": ("graph: replays of a captured step, one launch per pass" if args.graph
+                                else "persistent: one cooperative launch runs the T passes" if persistent
                                 else "stream: one launch per pass"),
                      "bytes_per_pass": bytes_per_pass, "avg_pass_us": avg_pass_s * 1e6,
                      "passes_per_launch": T if persistent else 1},
