@@ -24,6 +24,8 @@
 // multiple of 2^shift (the column's lowest set bit, fixed by the packer),
 // integers are added in any order, and the total is rounded once to binary64
 // (round-to-nearest-even).  No floating-point atomics are used.
+#include <type_traits>
+
 #include "esp_device.hpp"
 
 #pragma clang fp contract(off)
@@ -372,15 +374,21 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         const int tl = ai.reverse ? last - t : t;
         double best = 0.0;
         int bi = 0;
+        // The lane's best of its 4 entries (lowest index on ties); the
+        // penalty test is taken once per tile (a uniform branch), not per entry.
+        auto lane_best = [&](auto pen) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            double rent = static_cast<double>(d[0][i]) * lam[0];
+            for (int i = 0; i < 4; ++i) {
+                double rent = static_cast<double>(d[0][i]) * lam[0];
 #pragma unroll
-            for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
-            double sc = static_cast<double>(u[i]) - rent;
-            if (a.has_pen) sc = penalize(sc, pn[i], sw);
-            if (i == 0 || sc > best) { best = sc; bi = i; }
-        }
+                for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
+                double sc = static_cast<double>(u[i]) - rent;
+                if constexpr (decltype(pen)::value) sc = penalize(sc, pn[i], sw);
+                if (i == 0 || sc > best) { best = sc; bi = i; }
+            }
+        };
+        if (a.has_pen) lane_best(std::true_type{});
+        else lane_best(std::false_type{});
         int k = gl * 4 + bi;
         group_argmax<LPJ>(best, k);
         const int j = tl * JPT + jt;
@@ -581,14 +589,19 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         const int tl = ai.reverse ? last - t : t;
         const uint32_t hbits = (hw >> hshift) & 0xFu;
         double sc[4];
+        // the penalty test is taken once per tile (a uniform branch)
+        auto scores = [&](auto pen) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            double rent = static_cast<double>(d[0][i]) * lam[0];
+            for (int i = 0; i < 4; ++i) {
+                double rent = static_cast<double>(d[0][i]) * lam[0];
 #pragma unroll
-            for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
-            sc[i] = static_cast<double>(u[i]) - rent;
-            if (a.has_pen) sc[i] = penalize(sc[i], pn[i], sw);
-        }
+                for (int r = 1; r < R; ++r) rent = rent + static_cast<double>(d[r][i]) * lam[r];
+                sc[i] = static_cast<double>(u[i]) - rent;
+                if constexpr (decltype(pen)::value) sc[i] = penalize(sc[i], pn[i], sw);
+            }
+        };
+        if (a.has_pen) scores(std::true_type{});
+        else scores(std::false_type{});
         // Lane-local pass: the part before this lane's first head (it belongs to
         // a segment from lower lanes), segments complete inside the lane, and
         // the segment left open at the lane's end.
