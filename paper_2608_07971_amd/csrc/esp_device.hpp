@@ -41,7 +41,8 @@ __device__ __forceinline__ double dpp_d(double v) {
 // non-NaN scores the kernels produce, so any reduction tree returns the
 // entry a sequential lowest-index scan would.
 __device__ __forceinline__ void take_better(double &s, int &k, double os, int ok) {
-    const bool b = (os > s) || (os == s && ok < k);
+    // bitwise, not short-circuit, operators: no branches where lanes diverge
+    const bool b = (os > s) | ((os == s) & (ok < k));
     s = b ? os : s;
     k = b ? ok : k;
 }

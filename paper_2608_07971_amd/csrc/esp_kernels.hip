@@ -533,10 +533,11 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
     const double os = dpp_or_d<CTRL, ROW_MASK>(-__builtin_inf(), s);
     const int ok = dpp_or_i<CTRL, ROW_MASK>(0x7fffffff, k);
     const int of = dpp_or_i<CTRL, ROW_MASK>(0, f);
-    if (!f) {
-        take_better(s, k, os, ok);
-        f = of;
-    }
+    // selects and bitwise operators, not branches (the lanes diverge on f)
+    const bool take = (f == 0) & ((os > s) | ((os == s) & (ok < k)));
+    s = take ? os : s;
+    k = take ? ok : k;
+    f = f | of;
 }
 
 template <int R, typename A, int Mode>
@@ -609,20 +610,21 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         int pre_k = 0x7fffffff, cur_k = 0x7fffffff;
         bool has_pre = false, open = false;
         uint32_t local_win = 0;
+        // (selects, not branches: the lanes diverge on their head bits)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int slot = lane * 4 + i;
-            if ((hbits >> i) & 1u) {
-                if (open) local_win |= 1u << (cur_k - lane * 4);
-                open = true;
-                cur_s = sc[i];
-                cur_k = slot;
-            } else if (open) {
-                if (sc[i] > cur_s) { cur_s = sc[i]; cur_k = slot; }
-            } else {
-                if (!has_pre || sc[i] > pre_s) { pre_s = sc[i]; pre_k = slot; }
-                has_pre = true;
-            }
+            const bool head = (hbits >> i) & 1u;
+            // the previous segment ends here
+            local_win |= (head & open) ? (1u << ((cur_k - lane * 4) & 3)) : 0u;
+            const bool to_cur = head | (open & (sc[i] > cur_s));
+            cur_s = to_cur ? sc[i] : cur_s;
+            cur_k = to_cur ? slot : cur_k;
+            const bool to_pre = !head & !open & (!has_pre | (sc[i] > pre_s));
+            pre_s = to_pre ? sc[i] : pre_s;
+            pre_k = to_pre ? slot : pre_k;
+            has_pre = has_pre | (!head & !open);
+            open = open | head;
         }
         const bool has_head = hbits != 0;
         double ps = has_head ? cur_s : pre_s;
