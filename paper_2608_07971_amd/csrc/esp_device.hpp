@@ -88,8 +88,7 @@ __device__ __forceinline__ A fx_of(float v, int sh) {
     const uint32_t e = bits >> 23;
     const uint32_t m = (bits & 0x7fffffu) | (e ? 0x800000u : 0u);
     int s = (e ? static_cast<int>(e) : 1) - 150 - sh;
-    if (m == 0) return 0;
-    s = s > kMax ? kMax : (s < -kMax ? -kMax : s);
+    s = s > kMax ? kMax : (s < -kMax ? -kMax : s);       // (zero: m = 0 shifts to 0 either way)
     const A mm = m;
     return s >= 0 ? (mm << s) : (mm >> (-s));
 }

@@ -392,7 +392,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         int k = gl * 4 + bi;
         group_argmax<LPJ>(best, k);
         const int j = tl * JPT + jt;
-        const bool owner = ((k >> 2) == gl) && (j < ai.N);  // this lane holds the winning entry
+        const bool owner = ((k >> 2) == gl) & (j < ai.N);   // this lane holds the winning entry
         if (ai.choice && owner) ai.choice[static_cast<size_t>(cl) * ai.N + j] = k;
         if (ai.reduce) {
             const int w = k & 3;
@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
                 const float hi = (w & 1) ? d[r][3] : d[r][2];
                 v[r] = (w & 2) ? hi : lo;
             }
-            if (!(j < ai.N) && gl == 0) {
+            if ((j >= ai.N) & (gl == 0)) {
 #pragma unroll
                 for (int r = 0; r < R; ++r) s_stage[wave][jt][r] = 0.0f;   // jobs past N add nothing
             }
@@ -644,7 +644,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         if (lane < 8) s_win[wave][lane] = 0u;
         wave_sync();
         if (local_win) atomicOr(&s_win[wave][lane >> 3], local_win << hshift);
-        if (has_head && lane > 0) {
+        if (has_head & (lane > 0)) {
             if (has_pre) take_better(qs, qk, pre_s, pre_k);
             atomicOr(&s_win[wave][qk >> 5], 1u << (qk & 31));
         }
