@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs 
 #pragma unroll
                 for (int r = 0; r < R; ++r) mn[r] = kInf;
             }
-            const bool valid = (u[i] != -__builtin_inff()) && (jt < njobs);
+            const bool valid = (u[i] != -__builtin_inff()) & (jt < njobs);
             if (valid) {
 #pragma unroll
                 for (int r = 0; r < R; ++r) mn[r] = min(mn[r], __float_as_uint(d[r][i]));
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs 
             for (int r = 0; r < R; ++r) {
                 const uint32_t m = s_min[wave][q][r];
                 s_min[wave][q][r] = kInf;
-                if (take && m != kInf) acc[r] += fx_of<A>(__uint_as_float(m), sh[r]);
+                if (take & (m != kInf)) acc[r] += fx_of<A>(__uint_as_float(m), sh[r]);
             }
         }
         wave_sync();
@@ -173,11 +173,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
          gi += stride) {
         const int f = na.family[gi];
         float q[R];
-        bool ok = f >= 0 && f < a.N;
+        bool ok = (f >= 0) & (f < a.N);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             q[r] = na.query[gi * R + r];
-            ok = ok && (fabsf(q[r]) <= 3.402823466e38f);     // false for NaN and +-inf
+            ok = ok & (fabsf(q[r]) <= 3.402823466e38f);      // false for NaN and +-inf
         }
         int size = 0;
         const float *base = nullptr;       // the family's first entry (AOS) or its slot in column 0
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
             // within a lane, so keeping the first of equal distances keeps the
             // lowest index.  Selects, not a branch: all of the entry's loads
             // are issued before the mask is tested.
-            const bool take = d[0] != -__builtin_inff() && -acc > best;
+            const bool take = (d[0] != -__builtin_inff()) & (-acc > best);
             best = take ? -acc : best;
             bk = take ? k : bk;
             bu = take ? d[0] : bu;
