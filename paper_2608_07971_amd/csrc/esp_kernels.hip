@@ -46,24 +46,28 @@ __device__ __forceinline__ double step_size(const KArgs &a, int cl, int t) {
 
 // U_r from the cluster's exact total, the Eq. 8 update and the stop test for
 // resource r (one thread per resource of the cluster's last workgroup).
-template <int R>
-__device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r, u128 tot, int *s_ok,
-                                                  double *s_newlam) {
-    const bool bad = a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
+// lam_cur (LDS) holds the prices the iteration selected at.  Gather: the
+// launch is esp_reduce_demand's, whose workgroups flag invalid choices
+// (flag 4) during the launch; no other launch sets that flag.  An update
+// (lam_out set) happens only with one workgroup per cluster (deferred
+// completion otherwise), so the prices, the trace rows and the iteration
+// count each have one writer in a launch; the next launch reads them after
+// the launch boundary: plain stores.
+template <int R, bool Gather>
+__device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r, u128 tot, const double *lam_cur,
+                                                  int *s_ok, double *s_newlam) {
+    const bool bad =
+        Gather && a.flags && (__hip_atomic_load(&a.flags[cl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & 4);
     const double U = bad ? __builtin_nan("") : fx_to_double(tot, a.shift[cl * R + r]);
     if (a.demand_out) a.demand_out[cl * R + r] = U;
     if (a.tr_U) a.tr_U[cl * R + r] = U;
     int ok = 1;
     if (a.lam_out) {
-        const double lo = a.lam_in[cl * R + r];
+        const double lo = lam_cur[r];
         const double g = U - a.cap[cl * R + r];
         const double x = lo + step_size(a, cl, a.t) * g;
         const double ln = (x > 0.0) ? x : 0.0;
-        // agent-scope exchange: performed at the coherence point, where the
-        // next launch reads it
-        const double prev = __hip_atomic_exchange(&a.lam_out[cl * R + r], ln, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-        asm volatile("s_waitcnt vmcnt(0)" : : "v"(prev) : "memory");
+        a.lam_out[cl * R + r] = ln;
         if (a.tr_lam) a.tr_lam[cl * R + r] = ln;
         s_newlam[r] = ln;
         const double diff = fabs(ln - lo);
@@ -75,15 +79,12 @@ __device__ __forceinline__ void complete_resource(const KArgs &a, int cl, int r,
 
 // Per-cluster bookkeeping after the update (thread 0 of the last workgroup).
 // Returns whether the cluster stops (tol reached).
-template <int R>
+template <int R, bool Gather>
 __device__ __forceinline__ int complete_cluster(const KArgs &a, int cl, const int *s_ok) {
     int stop = 0;
-    if (a.flags && (a.flags[cl] & 4)) atomicAnd(&a.flags[cl], ~4);
+    if (Gather && a.flags && (a.flags[cl] & 4)) atomicAnd(&a.flags[cl], ~4);
     if (a.lam_out) {
-        // one writer per iteration, but not the same workgroup (or XCD) every
-        // time: a coherent exchange, so the last iteration's value is the one kept
-        if (a.iters_done) (void)__hip_atomic_exchange(&a.iters_done[cl], a.iter_no, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
+        if (a.iters_done) a.iters_done[cl] = a.iter_no;
         int all = 1;
         for (int r = 0; r < R; ++r) all &= s_ok[r];
         if (a.tol > 0.0 && all && a.flags) {
@@ -97,14 +98,15 @@ __device__ __forceinline__ int complete_cluster(const KArgs &a, int cl, const in
 // The demand sums of one iteration: U, the Eq. 8 update and the per-cluster
 // bookkeeping in the last workgroup.  s_newlam / s_stop (LDS) receive the new
 // prices and the stop decision there.
-template <int R>
-__device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum, double *s_newlam, int *s_stop) {
+template <int R, bool Gather>
+__device__ bool finish_cluster(const KArgs &a, int cl, int blk, const u128 *bsum, const double *lam_cur,
+                               double *s_newlam, int *s_stop) {
     __shared__ int s_ok[R];
     const bool last = cluster_sums<R>(a, cl, blk, bsum, [&](int r, u128 tot) {
-        complete_resource<R>(a, cl, r, tot, s_ok, s_newlam);
+        complete_resource<R, Gather>(a, cl, r, tot, lam_cur, s_ok, s_newlam);
     });
     if (!last) return false;
-    if (threadIdx.x == 0) *s_stop = complete_cluster<R>(a, cl, s_ok);
+    if (threadIdx.x == 0) *s_stop = complete_cluster<R, Gather>(a, cl, s_ok);
     __syncthreads();
     return true;
 }
@@ -486,7 +488,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
             __syncthreads();
         } else {
-            finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+            finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;
             prefetch_two(rev ^ a.sweep_alt);
             if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
@@ -762,7 +764,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
             __syncthreads();
         } else {
-            finish_cluster<R>(ai, cl, blk, s_bsum, s_newlam, &s_stop);
+            finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;
             load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
             if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
@@ -827,7 +829,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_gather(KArgs a) {
     }
     __shared__ double s_newlam[R];
     __shared__ int s_stop;
-    finish_cluster<R>(a, cl, blk, s_bsum, s_newlam, &s_stop);
+    finish_cluster<R, true>(a, cl, blk, s_bsum, nullptr, s_newlam, &s_stop);
 }
 
 // ---------------------------------------------------------------------------
