@@ -465,14 +465,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
         if (threadIdx.x < kBlockWaves * R) {
             const int w = threadIdx.x / R, r = threadIdx.x % R;
             u128 v = 0;
-#pragma unroll 1
+#pragma unroll   // independent LDS loads, all in flight
             for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
             s_wsum[w][r] = v;
         }
         __syncthreads();
         if (threadIdx.x < R) {
             u128 v = 0;
-#pragma unroll 1
+#pragma unroll
             for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
             s_bsum[threadIdx.x] = v;
         }
@@ -488,9 +488,10 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
             __syncthreads();
         } else {
+            // the next iteration's first tiles do not depend on the prices
+            if (Mode == kPersistLocal && it + 1 < a.n_iters) prefetch_two(rev ^ a.sweep_alt);
             finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;
-            prefetch_two(rev ^ a.sweep_alt);
             if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
         }
 #pragma unroll
@@ -741,14 +742,14 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         if (threadIdx.x < kBlockWaves * R) {
             const int w = threadIdx.x / R, r = threadIdx.x % R;
             u128 v = 0;
-#pragma unroll 1
+#pragma unroll   // independent LDS loads, all in flight
             for (int q = 0; q < Q; ++q) v += s_acc[w * kWaveSize + q * R + r];
             s_wsum[w][r] = v;
         }
         __syncthreads();
         if (threadIdx.x < R) {
             u128 v = 0;
-#pragma unroll 1
+#pragma unroll
             for (int w = 0; w < kBlockWaves; ++w) v += s_wsum[w][threadIdx.x];
             s_bsum[threadIdx.x] = v;
         }
@@ -764,9 +765,11 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
             if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
             __syncthreads();
         } else {
+            // the next iteration's first tile does not depend on the prices
+            if (Mode == kPersistLocal && it + 1 < a.n_iters)
+                load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
             finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;
-            load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
             if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
         }
 #pragma unroll
