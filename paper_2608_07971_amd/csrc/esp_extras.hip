@@ -321,8 +321,8 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
     }
     // Lane c < nblk keeps block c's summary in registers: largest residual
     // memory and compute over its GPUs that can still take a job, fewest
-    // jobs.  A block failing any of the three cannot hold the share, so
-    // skipping it is exact.
+    // jobs, or bounds on them (upper, upper, lower).  A block failing any of
+    // the three cannot hold the share, so skipping it is exact.
     double sum_m = m.gpu_memory, sum_s = m.gpu_compute;
     int sum_c = lane < nblk ? 0 : kMaxPerGpu;
     wave_sync();
@@ -353,17 +353,20 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
             const double nm = lane_d(nm_l, t);
             const double ns = lane_d(ns_l, t);
             uint64_t cand = __ballot((sum_c < kMaxPerGpu) & (sum_m >= nm) & (sum_s >= ns));
-            int found = 0;
-            while (cand != 0ull && found < g) {
-                const int c = __builtin_ctzll(cand);
+            int found = 0, visited = 0;
+            // the last visited block's GPUs of this lane, and which of them fit
+            int c = 0, h0 = 0, before = 0;
+            bool fit[kPerLane];
+            int cv[kPerLane];
+            double mv[kPerLane], sv[kPerLane];
+            while ((cand != 0ull) & (found < g)) {
+                c = __builtin_ctzll(cand);
                 cand &= cand - 1ull;
+                ++visited;
                 // lane l tests GPUs c*256 + 4l .. 4l+3 (ascending with the lane)
-                const int h0 = c * kStep + lane * kPerLane;
-                bool fit[kPerLane];
-                uint64_t bal[kPerLane];
-                int before = 0, total = 0;
-                int cv[kPerLane];
-                double mv[kPerLane], sv[kPerLane];
+                h0 = c * kStep + lane * kPerLane;
+                int total = 0;
+                before = 0;
 #pragma unroll
                 for (int i = 0; i < kPerLane; ++i) {
                     cv[i] = s_cnt[h0 + i];
@@ -373,9 +376,9 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
 #pragma unroll
                 for (int i = 0; i < kPerLane; ++i) {
                     fit[i] = (cv[i] < kMaxPerGpu) & (mv[i] >= nm) & (sv[i] >= ns);
-                    bal[i] = __ballot(fit[i]);
-                    before += __popcll(bal[i] & below);
-                    total += __popcll(bal[i]);
+                    const uint64_t bal = __ballot(fit[i]);
+                    before += __popcll(bal & below);
+                    total += __popcll(bal);
                 }
                 int rank = found + before;
 #pragma unroll
@@ -385,10 +388,54 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
                         ++rank;
                     }
                 }
+                if (found + total < g) {
+                    // the block cannot complete the share: make its summary
+                    // exact from the values just read
+                    double xm = -__builtin_inf(), xs = -__builtin_inf();
+                    int xc = kMaxPerGpu;
+#pragma unroll
+                    for (int i = 0; i < kPerLane; ++i) {
+                        const bool open = cv[i] < kMaxPerGpu;
+                        xm = open ? fmax(xm, mv[i]) : xm;
+                        xs = open ? fmax(xs, sv[i]) : xs;
+                        xc = min(xc, cv[i]);
+                    }
+                    wave_max2_min(xm, xs, xc);
+                    if (lane == c) {
+                        sum_m = xm;
+                        sum_s = xs;
+                        sum_c = xc;
+                    }
+                }
                 found += total;
             }
+            if (found < g) {                               // all or nothing
+                wave_sync();
+                continue;
+            }
+            if (visited == 1) {
+                // The share lies in one block: each selected GPU's lane updates
+                // it from the values it holds (no second round trip through
+                // LDS).  The block's summary is left as it was: residuals only
+                // shrink and counts only grow, so it stays an upper bound, and
+                // skipping the blocks it rules out stays exact; it is made exact
+                // again when a visit finds the block unable to complete a share.
+                int rank = before;
+#pragma unroll
+                for (int i = 0; i < kPerLane; ++i) {
+                    const bool take = fit[i] & (rank < g);
+                    rank += fit[i] ? 1 : 0;
+                    if (take) {
+                        s_mem[h0 + i] = mv[i] - nm;
+                        s_sm[h0 + i] = sv[i] - ns;
+                        s_occ[h0 + i][cv[i]] = j0 + t;
+                        s_cnt[h0 + i] = cv[i] + 1;
+                    }
+                }
+                wave_sync();
+                continue;
+            }
             wave_sync();
-            if (found < g) continue;                       // all or nothing
             if (lane < g) {
                 const int h = s_sel[lane];
                 const double mh = s_mem[h], sh_ = s_sm[h];
@@ -402,23 +449,23 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
             // refresh the summaries of the blocks that changed
             int last = -1;
             for (int i = 0; i < g; ++i) {
-                const int c = s_sel[i] / kStep;
-                if (c == last) continue;
-                last = c;
-                const int h0 = c * kStep + lane * kPerLane;
+                const int cb = s_sel[i] / kStep;
+                if (cb == last) continue;
+                last = cb;
+                const int hb = cb * kStep + lane * kPerLane;
                 double xm = -__builtin_inf(), xs = -__builtin_inf();
                 int xc = kMaxPerGpu;
 #pragma unroll
                 for (int q = 0; q < kPerLane; ++q) {
-                    const int cq = s_cnt[h0 + q];
-                    const double mq = s_mem[h0 + q], sq = s_sm[h0 + q];
+                    const int cq = s_cnt[hb + q];
+                    const double mq = s_mem[hb + q], sq = s_sm[hb + q];
                     const bool open = cq < kMaxPerGpu;           // GPUs that can still take a job
                     xm = open ? fmax(xm, mq) : xm;
                     xs = open ? fmax(xs, sq) : xs;
                     xc = min(xc, cq);
                 }
                 wave_max2_min(xm, xs, xc);
-                if (lane == c) {
+                if (lane == cb) {
                     sum_m = xm;
                     sum_s = xs;
                     sum_c = xc;
