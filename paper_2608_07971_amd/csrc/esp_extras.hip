@@ -252,8 +252,9 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
 //           placed in order; each lane tests 4 consecutive GPUs, so one step
 //           covers 256, only in blocks whose summary (largest residuals,
 //           fewest jobs) admits the share, and ballots rank the fitting
-//           GPUs.  Residuals live in LDS, updated in job order (binary64,
-//           the oracle's operations).
+//           GPUs.  A job needing at least as much as a share that already
+//           failed in this round is skipped without a scan.  Residuals live
+//           in LDS, updated in job order (binary64, the oracle's operations).
 //  IAC      every pair of jobs sharing a GPU: S_x|y = 1 + a_x b_y against
 //           tau_x = tau_base_x + min(beta (U / U_target - 1), beta_max),
 //           U = busy GPUs / G; a pair violates when either slowdown exceeds
@@ -325,6 +326,14 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
     // the three cannot hold the share, so skipping it is exact.
     double sum_m = m.gpu_memory, sum_s = m.gpu_compute;
     int sum_c = lane < nblk ? 0 : kMaxPerGpu;
+    // Lane l remembers a share that found no room in this round (GPU count,
+    // memory and compute per GPU; the lanes are filled in turn).  Residuals
+    // only shrink and counts only grow while jobs are placed, so a job that
+    // needs at least as much in all three as a remembered failure cannot be
+    // placed either: it is skipped without a scan.
+    int fail_g = 0x7fffffff;
+    double fail_m = __builtin_inf(), fail_s = __builtin_inf();
+    int n_fail = 0;
     wave_sync();
     const uint64_t below = (1ull << lane) - 1ull;
     // Jobs 64 at a time: each lane gathers one job's share (GPU count,
@@ -347,11 +356,22 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
             }
         }
         const int cnt = min(kWaveSize, N - j0);
+        // jobs of the batch already ruled out by the failures remembered so
+        // far (each lane tests its own job against every remembered one)
+        bool ruled_out = g_l == 0;
+        for (int f = 0; f < min(n_fail, kWaveSize); ++f) {
+            const int fg = lane_i(fail_g, f);
+            const double fm = lane_d(fail_m, f), fs = lane_d(fail_s, f);
+            ruled_out = ruled_out | ((g_l >= fg) & (nm_l >= fm) & (ns_l >= fs));
+        }
+        const uint64_t skip = __ballot(ruled_out);
         for (int t = 0; t < cnt; ++t) {
+            if ((skip >> t) & 1ull) continue;             // not placeable, or needs more than a failure
             const int g = lane_i(g_l, t);
-            if (g == 0) continue;                          // not placeable
             const double nm = lane_d(nm_l, t);
             const double ns = lane_d(ns_l, t);
+            // failures remembered within this batch
+            if (__ballot((g >= fail_g) & (nm >= fail_m) & (ns >= fail_s)) != 0ull) continue;
             uint64_t cand = __ballot((sum_c < kMaxPerGpu) & (sum_m >= nm) & (sum_s >= ns));
             int found = 0, visited = 0;
             // the last visited block's GPUs of this lane, and which of them fit
@@ -410,6 +430,12 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
                 found += total;
             }
             if (found < g) {                               // all or nothing
+                if (lane == (n_fail & (kWaveSize - 1))) {
+                    fail_g = g;
+                    fail_m = nm;
+                    fail_s = ns;
+                }
+                ++n_fail;
                 wave_sync();
                 continue;
             }
