@@ -526,18 +526,25 @@ __device__ __forceinline__ double dpp_or_d(double old, double v) {
         (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
 }
 
+// acc plus the number of set bits of a wave-wide mask in the lanes below this one.
+__device__ __forceinline__ unsigned below_lane(uint64_t m, unsigned acc) {
+    return __builtin_amdgcn_mbcnt_hi(static_cast<unsigned>(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo(static_cast<unsigned>(m), acc));
+}
+
 // One step of an inclusive segmented scan over lanes of (best score, slot,
 // segment-start flag): a lane without a segment start combines the value
-// arriving from lower lanes (lanes with no source receive the identity
-// (-inf, INT_MAX, 0)).  Lower slots come from lower lanes, so equal scores
-// keep the lower slot, as the sequential scan does.
+// arriving from lower lanes.  That value covers only slots below the lane's
+// own range, so on equal scores it is the one kept: the lowest slot wins, as
+// in the sequential scan, with no comparison of slots.  A lane with no source
+// receives its own (score, slot) and a clear flag, which changes nothing.
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
-    const double os = dpp_or_d<CTRL, ROW_MASK>(-__builtin_inf(), s);
-    const int ok = dpp_or_i<CTRL, ROW_MASK>(0x7fffffff, k);
+    const double os = dpp_or_d<CTRL, ROW_MASK>(s, s);
+    const int ok = dpp_or_i<CTRL, ROW_MASK>(k, k);
     const int of = dpp_or_i<CTRL, ROW_MASK>(0, f);
     // selects and bitwise operators, not branches (the lanes diverge on f)
-    const bool take = (f == 0) & ((os > s) | ((os == s) & (ok < k)));
+    const bool take = (f == 0) & (os >= s);
     s = take ? os : s;
     k = take ? ok : k;
     f = f | of;
@@ -640,32 +647,31 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         seg_scan_step<kDppRowBcast15, 0xa>(ps, pk, pf);
         seg_scan_step<kDppRowBcast31, 0xc>(ps, pk, pf);
         // Value of the scan at the previous lane (the segment that ends inside this lane).
-        double qs = dpp_or_d<kDppWaveShr1, 0xf>(-__builtin_inf(), ps);
-        int qk = dpp_or_i<kDppWaveShr1, 0xf>(0x7fffffff, pk);
+        const double qs = dpp_or_d<kDppWaveShr1, 0xf>(ps, ps);
+        int qk = dpp_or_i<kDppWaveShr1, 0xf>(pk, pk);
 
         // Winner mask of the tile (one bit per slot), built in LDS.
         if (lane < 8) s_win[wave][lane] = 0u;
         wave_sync();
         if (local_win) atomicOr(&s_win[wave][lane >> 3], local_win << hshift);
         if (has_head & (lane > 0)) {
-            if (has_pre) take_better(qs, qk, pre_s, pre_k);
-            atomicOr(&s_win[wave][qk >> 5], 1u << (qk & 31));
+            // the segment's part in this lane (before the first head) has the
+            // higher slots: it wins only with a strictly larger score
+            qk = (has_pre & (pre_s > qs)) ? pre_k : qk;
+            atomicOr(&s_win[wave][(qk >> 5) & 7], 1u << (qk & 31));
         }
-        if (lane == kWaveSize - 1) atomicOr(&s_win[wave][pk >> 5], 1u << (pk & 31));
+        if (lane == kWaveSize - 1) atomicOr(&s_win[wave][(pk >> 5) & 7], 1u << (pk & 31));
         wave_sync();
-        uint32_t wm[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) wm[q] = s_win[wave][q];
+        const uint32_t my_word = s_win[wave][lane >> 3];
         wave_sync();
-        const uint32_t wbits = (wm[lane >> 3] >> hshift) & 0xFu;
-        // Rank of this lane's first winner among the tile's winners (slot order).
-        int rank = __popc(wm[lane >> 3] & ((1u << hshift) - 1u));
-        int n_win = 0;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            n_win += __popc(wm[q]);
-            if (q < (lane >> 3)) rank += __popc(wm[q]);
-        }
+        const uint32_t wbits = (my_word >> hshift) & 0xFu;
+        // Rank of this lane's first winner among the tile's winners (slot
+        // order: lane, then entry): the winners in lower lanes, counted from
+        // one ballot per entry position; n_win is the same for every lane.
+        const uint64_t b0 = __ballot(wbits & 1u), b1 = __ballot(wbits & 2u);
+        const uint64_t b2 = __ballot(wbits & 4u), b3 = __ballot(wbits & 8u);
+        int rank = static_cast<int>(below_lane(b3, below_lane(b2, below_lane(b1, below_lane(b0, 0u)))));
+        const int n_win = __popcll(b0) + __popcll(b1) + __popcll(b2) + __popcll(b3);
         if (wbits) {
             uint32_t hwm[8];
             if (ai.choice) {
@@ -710,11 +716,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         }
     };
     // One tile of prefetch: the next tile's loads are in flight while the
-    // current one is scored (the loop body is large; unrolling it costs more
-    // than the deeper prefetch gains).
-    f4 nu, npn = {};
-    f4 nd[R];
-    uint32_t nhw = 0;
+    // current one is scored (a deeper prefetch measured no faster).  Two
+    // register sets take turns (the loop body appears twice), so the
+    // prefetched tile is scored where it landed, without copies.
+    f4 nu, npn = {}, bu, bpn = {};
+    f4 nd[R], bd[R];
+    uint32_t nhw = 0, bhw = 0;
     const int tile0 = blk * kBlockWaves + wave;
     Pending<R, A> pend;
     pending_loads<R, A>(a, cl, conv, pend);    // issued first: they return first
@@ -725,14 +732,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
     for (int it = 0; it < a.n_iters; ++it) {
         const KArgs ai = iteration_args<R>(a, it);
         const int rev = ai.reverse;
-        for (int tile = tile0; tile < a.tiles; tile += stride) {
-            const f4 u = nu, pn = npn;
-            f4 d[R];
-#pragma unroll
-            for (int r = 0; r < R; ++r) d[r] = nd[r];
-            const uint32_t hw = nhw;
-            load_tile(min(tile + stride, last), rev, nu, nd, npn, nhw);   // clamped: no branch
-            process(ai, tile, u, d, pn, hw);
+        for (int tile = tile0; tile < a.tiles; tile += 2 * stride) {
+            load_tile(min(tile + stride, last), rev, bu, bd, bpn, bhw);   // clamped: no branch
+            process(ai, tile, nu, nd, npn, nhw);
+            if (tile + stride >= a.tiles) break;
+            load_tile(min(tile + 2 * stride, last), rev, nu, nd, npn, nhw);
+            process(ai, tile + stride, bu, bd, bpn, bhw);
         }
         if (!ai.reduce) return;
 
