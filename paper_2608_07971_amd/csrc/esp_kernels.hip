@@ -550,8 +550,11 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
     f = f | of;
 }
 
+// Two wavefronts per SIMD at least (at most 256 registers): the CSR grid holds
+// two workgroups per CU, and a cooperative launch needs them all resident
+// (the persistent instances at R = 8 would otherwise take a few more).
 template <int R, typename A, int Mode>
-__global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
+__global__ __launch_bounds__(kBlockThreads, 2) void k_csr(KArgs a) {
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
     __shared__ uint32_t s_win[kBlockWaves][8];
     __shared__ float s_stage[kBlockWaves][kTileEntries][R];
@@ -613,32 +616,35 @@ __global__ __launch_bounds__(kBlockThreads) void k_csr(KArgs a) {
         };
         if (a.has_pen) scores(std::true_type{});
         else scores(std::false_type{});
-        // Lane-local pass: the part before this lane's first head (it belongs to
-        // a segment from lower lanes), segments complete inside the lane, and
+        // Lane-local pass: one running best (lowest entry on ties) that
+        // restarts at every head.  At a head the run so far is either a
+        // segment that began at an earlier head of this lane (complete: its
+        // winner is marked) or, before the lane's first head, this lane's
+        // part of a segment from lower lanes (pre).  At the end the run is
         // the segment left open at the lane's end.
-        double pre_s = -__builtin_inf(), cur_s = -__builtin_inf();
-        int pre_k = 0x7fffffff, cur_k = 0x7fffffff;
-        bool has_pre = false, open = false;
-        uint32_t local_win = 0;
         // (selects, not branches: the lanes diverge on their head bits)
+        const bool h0 = hbits & 1u;
+        double run_s = sc[0], pre_s = sc[0];
+        int run_i = 0, pre_i = 0;
+        bool open = h0;
+        uint32_t local_win = 0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int slot = lane * 4 + i;
+        for (int i = 1; i < 4; ++i) {
             const bool head = (hbits >> i) & 1u;
-            // the previous segment ends here
-            local_win |= (head & open) ? (1u << ((cur_k - lane * 4) & 3)) : 0u;
-            const bool to_cur = head | (open & (sc[i] > cur_s));
-            cur_s = to_cur ? sc[i] : cur_s;
-            cur_k = to_cur ? slot : cur_k;
-            const bool to_pre = !head & !open & (!has_pre | (sc[i] > pre_s));
-            pre_s = to_pre ? sc[i] : pre_s;
-            pre_k = to_pre ? slot : pre_k;
-            has_pre = has_pre | (!head & !open);
+            local_win |= static_cast<uint32_t>(head & open) << run_i;
+            const bool first = head & !open;
+            pre_s = first ? run_s : pre_s;
+            pre_i = first ? run_i : pre_i;
+            const bool take = head | (sc[i] > run_s);
+            run_s = take ? sc[i] : run_s;
+            run_i = take ? i : run_i;
             open = open | head;
         }
         const bool has_head = hbits != 0;
-        double ps = has_head ? cur_s : pre_s;
-        int pk = has_head ? cur_k : pre_k;
+        const bool has_pre = has_head & !h0;
+        const int pre_k = lane * 4 + pre_i;
+        double ps = run_s;
+        int pk = lane * 4 + run_i;
         int pf = has_head ? 1 : 0;
         seg_scan_step<kDppRowShr1, 0xf>(ps, pk, pf);
         seg_scan_step<kDppRowShr2, 0xf>(ps, pk, pf);

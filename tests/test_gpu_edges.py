@@ -38,7 +38,10 @@ def test_every_resource_count(R, layout):
     inst = (workloads.random_small(60 + R, 900, 8, R, dense=True, iters=40) if layout == "dense_k8"
             else workloads.random_small(70 + R, 700, 23, R, iters=40))
     _say(f"R={R} {layout}")
-    _parity(inst, 40)
+    # both drivers explicitly: the persistent one is a cooperative launch of
+    # the whole grid, which the kernel's registers must let the device hold
+    for mode in (esp.ESP_MODE_STREAM, esp.ESP_MODE_PERSISTENT):
+        _parity(inst, 40, mode)
 
 
 @pytest.mark.parametrize("layout", ["dense", "csr"])
@@ -67,13 +70,14 @@ def _wide(inst, seed, span=36):
     return inst
 
 
-@pytest.mark.parametrize("layout", ["dense_k16", "dense_k64_r8", "csr", "csr_batched"])
+@pytest.mark.parametrize("layout", ["dense_k16", "dense_k64_r8", "csr", "csr_batched", "csr_r8"])
 def test_wide_spans_use_128_bit_sums(layout):
     inst = {
         "dense_k16": lambda: workloads.random_small(90, 3000, 16, 5, dense=True, iters=60),
         "dense_k64_r8": lambda: workloads.random_small(91, 700, 64, 8, dense=True, iters=60),
         "csr": lambda: workloads.random_small(92, 2500, 30, 6, iters=60),
         "csr_batched": lambda: workloads.random_small(93, 800, 30, 4, n_clusters=3, iters=60),
+        "csr_r8": lambda: workloads.random_small(94, 1200, 40, 8, iters=60),
     }[layout]()
     _wide(inst, 5)
     inst.eta0 = np.full(inst.B, 1e-12)                   # prices stay in a useful range for 2^36 demands
