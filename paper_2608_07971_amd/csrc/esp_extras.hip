@@ -338,23 +338,48 @@ __global__ __launch_bounds__(kWaveSize) void k_pack_iac(KArgs a, IacArgs m) {
     const uint64_t below = (1ull << lane) - 1ull;
     // Jobs 64 at a time: each lane gathers one job's share (GPU count,
     // memory and compute per GPU), then the wavefront places them in order.
+    // The gathers run one batch ahead: while a batch is placed (LDS and
+    // registers only), the next batch's table values and the choices and
+    // family slots of the batch after it are in flight.  Indices past N are
+    // clamped (loaded, then ignored), so every load stays in bounds.
+    auto job_entry = [&](int j0, int &k, size_t &base) {
+        const int jl = min(j0 + lane, N - 1);
+        k = ch[jl];
+        base = a.K > 0 ? static_cast<size_t>(jl) * a.K : static_cast<size_t>(a.jobs[jl].slot);
+    };
+    auto share_of = [&](int k, size_t base, float &gv, float &mv, float &sv) {
+        const size_t e = base + static_cast<size_t>(k > 0 ? k : 0);
+        gv = col[(m.r_gpus + 1) * a.col_len + e];
+        mv = col[(m.r_mem + 1) * a.col_len + e];
+        sv = col[(m.r_sm + 1) * a.col_len + e];
+    };
+    int k_cur, k_next;
+    size_t b_cur, b_next;
+    float gv_cur, mv_cur, sv_cur;
+    job_entry(0, k_cur, b_cur);
+    share_of(k_cur, b_cur, gv_cur, mv_cur, sv_cur);
+    job_entry(kWaveSize, k_next, b_next);
     for (int j0 = 0; j0 < N; j0 += kWaveSize) {
+        float gv_n, mv_n, sv_n;
+        share_of(k_next, b_next, gv_n, mv_n, sv_n);
+        int k_after;
+        size_t b_after;
+        job_entry(j0 + 2 * kWaveSize, k_after, b_after);
         int g_l = 0;
         double nm_l = 0.0, ns_l = 0.0;
-        const int jl = j0 + lane;
-        if (jl < N) {
-            const int k = ch[jl];
-            if (k >= 0) {
-                const size_t e =
-                    (a.K > 0 ? static_cast<size_t>(jl) * a.K : static_cast<size_t>(a.jobs[jl].slot)) + k;
-                const double gv = static_cast<double>(col[(m.r_gpus + 1) * a.col_len + e]);
-                if (gv >= 1.0 && gv <= static_cast<double>(kMaxShards) && gv == floor(gv)) {
-                    g_l = static_cast<int>(gv);
-                    nm_l = static_cast<double>(col[(m.r_mem + 1) * a.col_len + e]) / gv;
-                    ns_l = static_cast<double>(col[(m.r_sm + 1) * a.col_len + e]) / gv;
-                }
-            }
+        const double gv = static_cast<double>(gv_cur);
+        if ((j0 + lane < N) & (k_cur >= 0) & (gv >= 1.0) & (gv <= static_cast<double>(kMaxShards)) &
+            (gv == floor(gv))) {
+            g_l = static_cast<int>(gv);
+            nm_l = static_cast<double>(mv_cur) / gv;
+            ns_l = static_cast<double>(sv_cur) / gv;
         }
+        k_cur = k_next;
+        gv_cur = gv_n;
+        mv_cur = mv_n;
+        sv_cur = sv_n;
+        k_next = k_after;
+        b_next = b_after;
         const int cnt = min(kWaveSize, N - j0);
         // jobs of the batch already ruled out by the failures remembered so
         // far (each lane tests its own job against every remembered one)
