@@ -196,7 +196,9 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
  * with several workgroups per cluster the update of iteration t is computed
  * at the start of the next pass, or of a closing launch after the last one),
  * then a re-selection at the final prices (Alg. 1).
- *   prices      device [B][R], in lambda^{t_start} (finite, >= 0), out the final prices
+ *   prices      device [B][R], in lambda^{t_start} (finite, >= 0; a -0.0 entry is stored
+ *               back as +0.0 before the first iteration, so no price the call
+ *               returns is -0.0), out the final prices
  *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
  * Graph capture: while `stream` is being captured, the iterations are
  * recorded as one launch each (ESP_MODE_AUTO falls back to it;
@@ -209,7 +211,11 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
  *   demand      device [B][R] or NULL: U at that selection
  *   trace       NULL or per-iteration records (see esp_trace)
  *   iters_done  device [B] int32 or NULL: updates made per cluster
- * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG, ESP_ERR_DEVICE.
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG (also: ESP_MODE_PERSISTENT while
+ * `stream` is being captured; nothing is enqueued or recorded then),
+ * ESP_ERR_DEVICE (a HIP call failed, or ESP_MODE_PERSISTENT with a grid the
+ * device cannot hold co-resident: refused on the host before the first
+ * iteration is launched).
  */
 esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_start, double tol,
                      int32_t *choice, double *demand, const esp_trace *trace, int32_t *iters_done,

@@ -275,7 +275,12 @@ class Oracle:
 
     # whole loop ---------------------------------------------------------
     def solve(self, lam0=None, iters: Optional[int] = None, t_start: int = 1, tol: float = 0.0,
-              trace: bool = True, trace_choice: bool = False) -> dict:
+              trace: bool = True, trace_choice: bool = False, duals: bool = True) -> dict:
+        """The loop of Sec. 3.2.3 from lam0 for `iters` iterations starting at
+        step index t_start.  trace: per-iteration prices and demand (and, with
+        duals, the dual and primal values); trace_choice: per-iteration
+        selections.  A solve continued from another's final prices with
+        t_start advanced reproduces the longer solve's iterates."""
         T = int(self.inst.iters if iters is None else iters)
         B, N, R = self.B, self.N, self.R
         lam = np.array(self.inst.lam0 if lam0 is None else lam0, dtype=np.float64).reshape(B, R).copy()
@@ -287,8 +292,9 @@ class Oracle:
         if trace:
             out["tr_lam"] = np.full((T, B, R), np.nan)
             out["tr_U"] = np.full((T, B, R), np.nan)
-            out["tr_dual"] = np.full((T, B), np.nan)
-            out["tr_primal"] = np.full((T, B), np.nan)
+            if duals:
+                out["tr_dual"] = np.full((T, B), np.nan)
+                out["tr_primal"] = np.full((T, B), np.nan)
         if trace_choice:
             out["tr_choice"] = np.full((T, B, N), -1, dtype=np.int32)
         rc = self.L.orc_solve(self._pp, _p(lam), T, t_start, tol,

@@ -596,7 +596,7 @@ esp_status esp_score_select(esp_ctx *c, const double *prices, int32_t *choice, v
     hipStream_t s = static_cast<hipStream_t>(stream);
     KArgs p = c->base;
     p.iters_done = nullptr;
-    if ((st = dev(launch_prepare(c->pl.R, p, prices, c->pl.B, s))) != ESP_OK) return st;
+    if ((st = dev(launch_prepare(c->pl.R, p, prices, nullptr, c->pl.B, s))) != ESP_OK) return st;
     KArgs a = c->base;
     a.lam_in = prices;
     a.choice = choice;
@@ -640,23 +640,27 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
     int32_t *d_iters = reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters);
+    // Persistent launches (one cooperative launch per chunk of up to
+    // kLaunchChunk iterations); one launch per iteration in stream mode, when
+    // the device cannot hold the grid co-resident, or while `stream` is being
+    // captured into a graph (a cooperative launch cannot be captured).  The
+    // capture is checked before anything is enqueued, so a refused call
+    // records nothing.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
     {
+        // validates the prices, turns -0.0 into +0.0 in place, resets the
+        // per-solve state
         KArgs p = c->base;
         p.iters_done = d_iters;
-        if ((st = dev(launch_prepare(R, p, prices, B, s))) != ESP_OK) return st;
+        if ((st = dev(launch_prepare(R, p, prices, prices, B, s))) != ESP_OK) return st;
     }
     // With several workgroups per cluster every iteration only publishes its
     // sums; the next launch (or the closing one) completes it.  With one
     // workgroup per cluster the workgroup completes its own iteration.
     const bool defer = c->pl.nblk > 1;
-    // Persistent launches (one cooperative launch per chunk of up to
-    // kLaunchChunk iterations); one launch per iteration in stream mode, when
-    // the device cannot hold the grid co-resident, or while `stream` is being
-    // captured into a graph (a cooperative launch cannot be captured).
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
-    const bool capturing = cap != hipStreamCaptureStatusNone;
-    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
     bool persistent =
         !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
     KArgs base = c->base;
@@ -702,8 +706,8 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
             const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
                                            : launch_dense_persistent(R, c->pl.lpj, a, B, s);
             if (e == hipSuccess) continue;
+            (void)hipGetLastError();           // not left for the next launch's error check
             if (!c->auto_mode) return ESP_ERR_DEVICE;
-            (void)hipGetLastError();
             persistent = false;                // fall back to one launch per iteration
             c->fell_back = true;
         }

@@ -123,13 +123,17 @@ constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
 
 // Host-side launchers (esp_kernels.hip).
 hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
-// Cooperative launch (all workgroups co-resident) of a multi-iteration dense launch.
+// Cooperative launch (all workgroups co-resident) of a multi-iteration dense
+// launch.  A grid the device cannot hold co-resident is refused on the host
+// (hipErrorCooperativeLaunchTooLarge) before anything is enqueued.
 hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
-hipError_t launch_prepare(int R, const KArgs &a, const double *lam, int B, hipStream_t s);
+// Validates prices `lam`; `canon` (NULL or the same buffer, writable) receives
+// +0.0 in place of -0.0.
+hipError_t launch_prepare(int R, const KArgs &a, const double *lam, double *canon, int B, hipStream_t s);
 // Closing launch of a deferred solve: completes its last iteration (no selection).
 hipError_t launch_finish(int R, const KArgs &a, int B, hipStream_t s);
 

@@ -875,21 +875,31 @@ __global__ void k_update(KArgs a, const double *demand_in, int B) {
     }
 }
 
-// Validate prices before a solve or a selection; mark bad clusters.  For a
+// Validate prices before a solve or a selection; mark bad clusters.  A valid
+// price -0.0 is stored back as +0.0 when `canon` is set (the solve's in/out
+// prices; never -0.0 afterwards, as after the projection of Eq. 8).  For a
 // solve (iters_done set) also reset the per-solve counters and store the
 // starting prices as lambda_1 (lam_ws[1]) for the first deferred completion.
 template <int R>
-__global__ void k_prepare(KArgs a, const double *lam, int B) {
+__global__ void k_prepare(KArgs a, const double *lam, double *canon, int B) {
     const int cl = blockIdx.x * blockDim.x + threadIdx.x;
     if (cl >= B) return;
     bool ok = true;
     for (int r = 0; r < R; ++r) ok = ok && price_ok(lam[cl * R + r]);
     a.flags[cl] = (a.flags[cl] & kFlagFrozen) | (ok ? 0 : kFlagError);
+    if (ok && canon) {
+        for (int r = 0; r < R; ++r)
+            if (__double_as_longlong(lam[cl * R + r]) == static_cast<long long>(0x8000000000000000ull))
+                canon[cl * R + r] = 0.0;
+    }
     if (a.iters_done) {
         a.iters_done[cl] = 0;
         for (int i = 0; i < kSyncSlots; ++i) a.sync[(static_cast<size_t>(cl) * kSyncSlots + i) * kSyncStride] = 0u;
         a.conv_at[cl] = 0;
-        for (int r = 0; r < R; ++r) a.lam_ws[static_cast<size_t>(B) * R + static_cast<size_t>(cl) * R + r] = lam[cl * R + r];
+        for (int r = 0; r < R; ++r) {
+            const double v = lam[cl * R + r];
+            a.lam_ws[static_cast<size_t>(B) * R + static_cast<size_t>(cl) * R + r] = (v == 0.0) ? 0.0 : v;
+        }
     }
     if (!ok) atomicCAS(a.status, 0, kStatusNonfinite);
 }
@@ -931,6 +941,20 @@ static hipError_t launch_dense_r(int lpj, const KArgs &a, int B, hipStream_t s) 
     return a.acc128 ? launch_dense_ra<R, u128>(lpj, a, B, s) : launch_dense_ra<R, uint64_t>(lpj, a, B, s);
 }
 
+// A cooperative launch of `blocks` workgroups of kernel f: refused on the host
+// when the device cannot hold them all at once (nothing is enqueued then).
+static hipError_t launch_cooperative(const void *f, unsigned blocks, const KArgs &a, hipStream_t s) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, f, kBlockThreads, 0) != hipSuccess)
+        return hipErrorInvalidValue;
+    if (static_cast<int64_t>(blocks) > static_cast<int64_t>(per_cu) * cus) return hipErrorCooperativeLaunchTooLarge;
+    KArgs copy = a;
+    void *args[] = {&copy};
+    return hipLaunchCooperativeKernel(f, dim3(blocks), dim3(kBlockThreads), args, 0, s);
+}
+
 template <int R, typename A>
 static hipError_t launch_dense_coop_ra(int lpj, const KArgs &a, int B, hipStream_t s) {
     const void *f = nullptr;
@@ -947,9 +971,7 @@ static hipError_t launch_dense_coop_ra(int lpj, const KArgs &a, int B, hipStream
                            : reinterpret_cast<const void *>(&k_dense<R, 16, A, kPersistLocal>); break;
         default: return hipErrorInvalidValue;
     }
-    KArgs copy = a;
-    void *args[] = {&copy};
-    return hipLaunchCooperativeKernel(f, dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), args, 0, s);
+    return launch_cooperative(f, static_cast<unsigned>(B) * a.nblk, a, s);
 }
 
 template <int R>
@@ -999,13 +1021,13 @@ hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, 
 }
 
 template <int R>
-static hipError_t launch_prepare_r(const KArgs &a, const double *lam, int B, hipStream_t s) {
-    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, a, lam, B);
+static hipError_t launch_prepare_r(const KArgs &a, const double *lam, double *canon, int B, hipStream_t s) {
+    hipLaunchKernelGGL((k_prepare<R>), dim3((B + 255) / 256), dim3(256), 0, s, a, lam, canon, B);
     return hipGetLastError();
 }
 
-hipError_t launch_prepare(int R, const KArgs &a, const double *lam, int B, hipStream_t s) {
-#define CALL(RR) launch_prepare_r<RR>(a, lam, B, s)
+hipError_t launch_prepare(int R, const KArgs &a, const double *lam, double *canon, int B, hipStream_t s) {
+#define CALL(RR) launch_prepare_r<RR>(a, lam, canon, B, s)
     ESP_DISPATCH_R(R, CALL)
 #undef CALL
 }
@@ -1039,9 +1061,7 @@ static hipError_t launch_csr_coop_r(const KArgs &a, int B, hipStream_t s) {
                                         : reinterpret_cast<const void *>(&k_csr<R, u128, kPersistLocal>))
                              : (a.defer ? reinterpret_cast<const void *>(&k_csr<R, uint64_t, kPersistDeferred>)
                                         : reinterpret_cast<const void *>(&k_csr<R, uint64_t, kPersistLocal>));
-    KArgs copy = a;
-    void *args[] = {&copy};
-    return hipLaunchCooperativeKernel(f, dim3(static_cast<unsigned>(B) * a.nblk), dim3(kBlockThreads), args, 0, s);
+    return launch_cooperative(f, static_cast<unsigned>(B) * a.nblk, a, s);
 }
 
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s) {

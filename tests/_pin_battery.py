@@ -29,6 +29,17 @@ def battery(L) -> None:
         assert list(res["choice"][0]) == [int(x) for x in g["final_choice"]]
         for x in res["tr_lam"].ravel():
             assert math.copysign(1.0, x) > 0
+    # early stop (hand_tol.txt): where a tolerance stops the loop
+    g = read_golden("hand_tol.txt")
+    o = oracle.Oracle(golden_instance(g), L)
+    res = o.solve(tol=g["tol"][0], trace_choice=True)
+    assert int(res["iters_done"][0]) == int(g["iters_done"][0])
+    for i, row in enumerate(g["trace"]):
+        assert np.array_equal(res["tr_lam"][i, 0], np.array(row[4]))
+    assert np.array_equal(res["lam"][0], np.array(g["final_lam"]))
+    for tol, n, lam in g["cases"]:
+        r = o.solve(tol=tol[0])
+        assert int(r["iters_done"][0]) == int(n[0]) and np.array_equal(r["lam"][0], np.array(lam))
     # step sizes
     assert oracle.eta(1, 0.01, 1, L) == 0.01 and oracle.eta(1, 1.0, 4, L) == 0.5
     assert oracle.eta(0, 0.3, 7, L) == 0.3

@@ -180,3 +180,34 @@ def test_case2_memory_price_rises_under_overload():
     first_fit = int(np.argmax(~over))
     assert not over[first_fit]
     assert (res["tr_choice"][first_fit, 0] > 0).any()      # some job moved off its peak config
+
+
+def test_hand_tol_stop_rule():
+    """The early-stop reading (hand_tol.txt): the oracle stops after the
+    first update where every resource's price change is within tol times
+    max(1, the pre-update price), reports that many updates, re-selects at
+    the prices reached, and leaves the later trace rows untouched."""
+    g = read_golden("hand_tol.txt")
+    inst = golden_instance(g)
+    o = oracle.Oracle(inst)
+    res = o.solve(tol=g["tol"][0], trace_choice=True)
+    done = int(g["iters_done"][0])
+    assert int(res["iters_done"][0]) == done
+    for i, row in enumerate(g["trace"]):
+        t, lam_t, ch, U, lam_next, dual, flags = row
+        assert np.array_equal(res["tr_U"][i, 0], np.array(U)), i
+        assert np.array_equal(res["tr_lam"][i, 0], np.array(lam_next)), i
+        assert res["tr_dual"][i, 0] == dual[0], i
+        # the stop test of the reading, from the fixture's own prices
+        ok = [abs(b - a) <= g["tol"][0] * max(1.0, a) for a, b in zip(lam_t, lam_next)]
+        assert ok == [bool(x) for x in flags], i
+    assert np.isnan(res["tr_lam"][done:]).all() and np.isnan(res["tr_U"][done:]).all()
+    assert list(res["choice"][0]) == [int(x) for x in g["final_choice"]]
+    assert np.array_equal(res["U"][0], np.array(g["final_U"]))
+    assert np.array_equal(res["lam"][0], np.array(g["final_lam"]))
+    for tol, n, lam in g["cases"]:
+        r = o.solve(tol=tol[0])
+        assert int(r["iters_done"][0]) == int(n[0]), tol
+        assert np.array_equal(r["lam"][0], np.array(lam)), tol
+    # tol = 0 runs every iteration
+    assert int(o.solve(tol=0.0)["iters_done"][0]) == inst.iters

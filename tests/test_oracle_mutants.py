@@ -62,6 +62,16 @@ MUTANTS = {
                         "x = (double)q[0]"),
     "nn_wrong_dim": ("x = (double)q[r] - (double)d[e * p->R + r];", "x = (double)q[r] - (double)d[e * p->R];"),
     "nn_estimate_first": ("util_of(p, b)[p->offsets[family[i]] + c]", "util_of(p, b)[p->offsets[family[i]]]"),
+    "stop_post_update_scale": ("double scale = prev[r] > 1.0 ? prev[r] : 1.0;",
+                               "double scale = lb[r] > 1.0 ? lb[r] : 1.0;"),
+    "stop_strict": ("if (!(diff <= tol * scale)) conv = 0;", "if (!(diff < tol * scale)) conv = 0;"),
+    "stop_absolute": ("double scale = prev[r] > 1.0 ? prev[r] : 1.0;", "double scale = 1.0;"),
+    "stop_no_unit_floor": ("double scale = prev[r] > 1.0 ? prev[r] : 1.0;", "double scale = prev[r];"),
+    "stop_any_resource": ("if (!(diff <= tol * scale)) conv = 0;\n                }\n                if (conv) break;",
+                          "if (diff <= tol * scale) conv = 2;\n                }\n                if (conv == 2) break;"),
+    "stop_step_not_change": ("double diff = fabs(lb[r] - prev[r]);", "double diff = fabs(eta * (U[r] - Cb[r]));"),
+    "stop_never": ("if (conv) break;", ";"),
+    "stop_count_off_by_one": ("done = i + 1;", "done = i;"),
     "ceff_whole_config": ("if (!have || v < m) { m = v; have = 1; }",
                           "if (!have || d[e * q->R] < d[(q->offsets[j]) * q->R]) { m = v; have = 1; }"),
 }
