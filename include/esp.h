@@ -222,6 +222,33 @@ esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_star
                      void *stream);
 
 /*
+ * esp_solve_noalloc: esp_solve for callers that cannot allocate memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Same arguments, results and errors as esp_solve (bit for bit
+ * the same outputs), but the call allocates nothing and its per-solve scratch
+ * -- per-workgroup partial sums, arrival tickets, barrier words, the prices of
+ * the iteration being completed, the stop iteration and the update counts --
+ * lives in one static device array of the library, ESP_NOALLOC_SCRATCH_BYTES
+ * on each GPU, held until the process ends, instead of the context's
+ * workspace (whose read-only parts -- the packed table, capacities, step
+ * scales -- it still reads, and whose status word and run flags it still
+ * uses).  Every call on one GPU shares that GPU's array, whatever the context:
+ * calls that overlap on one GPU race and must be serialized by the caller
+ * (one stream, or events).  The array keeps the last call's contents; what
+ * must start at zero is cleared by each call's first kernel.  The context
+ * must have been created with the GPU current that later calls run on.
+ * Errors: those of esp_solve, and ESP_ERR_WORKSPACE when the context's
+ * scratch (3 B nblk R 16 + B 4352 + 2 B R 8 bytes and alignment, nblk the
+ * workgroups per cluster) exceeds ESP_NOALLOC_SCRATCH_BYTES (B up to about
+ * 400 clusters at R = 8), ESP_ERR_DEVICE when the array's address could not
+ * be resolved at esp_create.
+ */
+#define ESP_NOALLOC_SCRATCH_BYTES (2u << 20)
+esp_status esp_solve_noalloc(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_start, double tol,
+                             int32_t *choice, double *demand, const esp_trace *trace, int32_t *iters_done,
+                             void *stream);
+
+/*
  * esp_device_status: wait for `stream`, then return (and clear) the first
  * error the GPU recorded since the last call: ESP_ERR_NONFINITE or
  * ESP_ERR_INVALID_ARG for prices that were NaN, infinite or negative (the

@@ -89,6 +89,8 @@ _SIGS = {
     "esp_update_prices": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p], C.c_int),
     "esp_solve": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_void_p,
                    C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
+    "esp_solve_noalloc": ([C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_void_p,
+                           C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_set_penalties": ([C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p], C.c_int),
     "esp_device_status": ([C.c_void_p, C.c_void_p], C.c_int),
     "esp_loop_driver": ([C.c_void_p, C.POINTER(C.c_int32)], C.c_int),
@@ -223,6 +225,13 @@ def esp_solve(ctx: int, prices, iters: int, t_start: int = 1, tol: float = 0.0, 
     _check(lib().esp_solve(ctx, _ptr(prices), int(iters), int(t_start), float(tol), _ptr(choice), _ptr(demand),
                            None if trace is None else C.addressof(trace), _ptr(iters_done), _stream(stream)),
            "esp_solve")
+
+
+def esp_solve_noalloc(ctx: int, prices, iters: int, t_start: int = 1, tol: float = 0.0, choice=None, demand=None,
+                      trace: Optional[esp_trace] = None, iters_done=None, stream=None) -> None:
+    _check(lib().esp_solve_noalloc(ctx, _ptr(prices), int(iters), int(t_start), float(tol), _ptr(choice),
+                                   _ptr(demand), None if trace is None else C.addressof(trace), _ptr(iters_done),
+                                   _stream(stream)), "esp_solve_noalloc")
 
 
 def esp_set_penalties(ctx: int, current=None, switch_cost=None, penalty=None, stream=None) -> None:

@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -201,8 +202,56 @@ struct PinnedPair {
 
 }  // namespace
 
+// Scratch of esp_solve_noalloc: one array per GPU, in the library's code
+// object, held until the process ends.  Host code never uses `scratch`
+// itself (on the host it is a stand-in, not a device address): each device's
+// address comes from hipGetSymbolAddress, resolved once per device with that
+// device current, when a context is created on it.
+static __device__ __align__(256) unsigned char scratch[ESP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (NULL when it cannot be resolved).
+char *resolve_scratch(int dev) {
+    if (dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) g_scratch_ptr[dev] = static_cast<char *>(p);
+        else (void)hipGetLastError();
+    }
+    return g_scratch_ptr[dev];
+}
+
+// Byte offsets of the per-solve scratch regions of a plan inside the static
+// array, each 256-byte aligned; the last value is the size.
+struct ScratchLayout {
+    size_t part = 0, tick = 0, iters = 0, sync = 0, lamws = 0, conv = 0, total = 0;
+};
+
+ScratchLayout scratch_layout(const Plan &pl) {
+    const size_t B = pl.B, R = pl.R;
+    ScratchLayout L;
+    size_t o = 0;
+    L.part = o;  o = align_up(o + kPartialBuffers * B * pl.nblk * R * 2 * sizeof(uint64_t));
+    L.tick = o;  o = align_up(o + B * sizeof(uint32_t));
+    L.iters = o; o = align_up(o + B * sizeof(int32_t));
+    L.sync = o;  o = align_up(o + B * kSyncSlots * kSyncStride * sizeof(uint32_t));
+    L.lamws = o; o = align_up(o + 2 * B * R * sizeof(double));
+    L.conv = o;  o = align_up(o + B * sizeof(int32_t));
+    L.total = o;
+    return L;
+}
+
+}  // namespace
+
 struct esp_ctx {
     uint32_t magic = kMagic;
+    char *scratch = nullptr;           // this device's address of `scratch`, or NULL
     Plan pl;
     int rule = 0;
     std::vector<double> eta0;
@@ -280,6 +329,125 @@ esp_status stage_wait(esp_ctx *c) {
 
 hipError_t launch_select(const esp_ctx *c, const KArgs &a, hipStream_t s) {
     return c->pl.csr ? launch_csr(c->pl.R, a, c->pl.B, s) : launch_dense(c->pl.R, c->pl.lpj, a, c->pl.B, s);
+}
+
+}  // namespace
+
+namespace {
+
+// The body of esp_solve and esp_solve_noalloc.  `kb` is the context's launch
+// arguments with the per-solve scratch (partial sums, tickets, barrier words,
+// lambda_m, stop iteration) pointing into the context's workspace or into the
+// static scratch array; d_iters (device [B]) counts the updates.
+esp_status solve_with(esp_ctx *c, const KArgs &kb, int32_t *d_iters, double *prices, int32_t iters,
+                      int32_t t_start, double tol, int32_t *choice, double *demand, const esp_trace *trace,
+                      int32_t *iters_done, void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    if (prices == nullptr || iters < 0 || t_start < 1 || !(tol >= 0.0) || !std::isfinite(tol))
+        return ESP_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(t_start) + iters - 1 > INT32_MAX) return ESP_ERR_INVALID_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
+    // Persistent launches (one cooperative launch per chunk of up to
+    // kLaunchChunk iterations); one launch per iteration in stream mode, when
+    // the device cannot hold the grid co-resident, or while `stream` is being
+    // captured into a graph (a cooperative launch cannot be captured).  The
+    // capture is checked before anything is enqueued, so a refused call
+    // records nothing.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
+    {
+        // validates the prices, turns -0.0 into +0.0 in place, resets the
+        // per-solve state
+        KArgs p = kb;
+        p.iters_done = d_iters;
+        if ((st = dev(launch_prepare(R, p, prices, prices, B, s))) != ESP_OK) return st;
+    }
+    // With several workgroups per cluster every iteration only publishes its
+    // sums; the next launch (or the closing one) completes it.  With one
+    // workgroup per cluster the workgroup completes its own iteration.
+    const bool defer = c->pl.nblk > 1;
+    bool persistent =
+        !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
+    KArgs base = kb;
+    base.lam_in = prices;
+    base.lam_dst = prices;
+    base.iters_done = d_iters;
+    base.tol = tol;
+    base.defer = defer ? 1 : 0;
+    if (defer) {
+        base.lam_out = nullptr;
+        base.skip_mask = kFlagError | kFlagFrozen;
+        if (trace) {
+            base.trace_lam = trace->prices;
+            base.trace_U = trace->demand;
+        }
+    } else {
+        base.lam_out = prices;
+        base.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
+    }
+    // Launch arguments for solve iterations i .. i + n - 1 (0-based).
+    auto iteration_launch = [&](int32_t i, int32_t n) {
+        KArgs a = base;
+        a.n_iters = n;
+        a.t = t_start + i;
+        a.iter_no = i + 1;
+        a.reduce = 1;
+        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i & 1) : 0;
+        if (defer && i > 0) {
+            a.pend_m = i;
+            a.pend_t = t_start + i - 1;
+        }
+        if (trace) {
+            if (!defer && trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(i) * B * R;
+            if (!defer && trace->demand) a.tr_U = trace->demand + static_cast<size_t>(i) * B * R;
+            if (trace->choice) a.choice = trace->choice + static_cast<size_t>(i) * B * N;
+        }
+        return a;
+    };
+    for (int32_t i0 = 0; i0 < iters; i0 += kLaunchChunk) {
+        const int n = std::min<int32_t>(kLaunchChunk, iters - i0);
+        if (persistent) {
+            const KArgs a = iteration_launch(i0, n);
+            const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
+                                           : launch_dense_persistent(R, c->pl.lpj, a, B, s);
+            if (e == hipSuccess) continue;
+            (void)hipGetLastError();           // not left for the next launch's error check
+            if (!c->auto_mode) return ESP_ERR_DEVICE;
+            persistent = false;                // fall back to one launch per iteration
+            c->fell_back = true;
+        }
+        for (int i = 0; i < n; ++i)
+            if ((st = dev(launch_select(c, iteration_launch(i0 + i, 1), s))) != ESP_OK) return st;
+    }
+    // Closing launch: completes the last iteration of a deferred solve, and
+    // re-selects at the final prices (no update) when asked to.
+    KArgs a = base;
+    a.lam_out = nullptr;
+    a.tr_lam = a.tr_U = nullptr;
+    a.defer = 0;
+    a.n_iters = 1;
+    a.skip_mask = kFlagError | kFlagFrozen;
+    if (defer && iters > 0) {
+        a.pend_m = iters;
+        a.pend_t = t_start + iters - 1;
+    }
+    if (choice || demand) {
+        a.choice = choice;
+        a.demand_out = demand;
+        a.reduce = demand ? 1 : 0;
+        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(iters & 1) : 0;
+        if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
+    } else if (a.pend_m > 0) {
+        if ((st = dev(launch_finish(R, a, B, s))) != ESP_OK) return st;
+    }
+    if (iters_done &&
+        hipMemcpyAsync(iters_done, d_iters, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return ESP_ERR_DEVICE;
+    return ESP_OK;
 }
 
 }  // namespace
@@ -393,6 +561,10 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     esp_ctx *c = new (std::nothrow) esp_ctx();
     if (c == nullptr) return ESP_ERR_DEVICE;
     c->pl = pl;
+    {
+        int dev = 0;
+        if (hipGetDevice(&dev) == hipSuccess) c->scratch = resolve_scratch(dev);
+    }
     c->rule = step->rule;
     c->eta0.assign(step->eta0, step->eta0 + B);
     c->ws = ws;
@@ -634,111 +806,26 @@ esp_status esp_solve(esp_ctx *c, double *prices, int32_t iters, int32_t t_start,
                      double *demand, const esp_trace *trace, int32_t *iters_done, void *stream) {
     esp_status st = check_ctx(c);
     if (st != ESP_OK) return st;
-    if (prices == nullptr || iters < 0 || t_start < 1 || !(tol >= 0.0) || !std::isfinite(tol))
-        return ESP_ERR_INVALID_ARG;
-    if (static_cast<int64_t>(t_start) + iters - 1 > INT32_MAX) return ESP_ERR_INVALID_ARG;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const int B = c->pl.B, R = c->pl.R, N = c->pl.N;
-    int32_t *d_iters = reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters);
-    // Persistent launches (one cooperative launch per chunk of up to
-    // kLaunchChunk iterations); one launch per iteration in stream mode, when
-    // the device cannot hold the grid co-resident, or while `stream` is being
-    // captured into a graph (a cooperative launch cannot be captured).  The
-    // capture is checked before anything is enqueued, so a refused call
-    // records nothing.
-    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
-    const bool capturing = cap != hipStreamCaptureStatusNone;
-    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
-    {
-        // validates the prices, turns -0.0 into +0.0 in place, resets the
-        // per-solve state
-        KArgs p = c->base;
-        p.iters_done = d_iters;
-        if ((st = dev(launch_prepare(R, p, prices, prices, B, s))) != ESP_OK) return st;
-    }
-    // With several workgroups per cluster every iteration only publishes its
-    // sums; the next launch (or the closing one) completes it.  With one
-    // workgroup per cluster the workgroup completes its own iteration.
-    const bool defer = c->pl.nblk > 1;
-    bool persistent =
-        !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
-    KArgs base = c->base;
-    base.lam_in = prices;
-    base.lam_dst = prices;
-    base.iters_done = d_iters;
-    base.tol = tol;
-    base.defer = defer ? 1 : 0;
-    if (defer) {
-        base.lam_out = nullptr;
-        base.skip_mask = kFlagError | kFlagFrozen;
-        if (trace) {
-            base.trace_lam = trace->prices;
-            base.trace_U = trace->demand;
-        }
-    } else {
-        base.lam_out = prices;
-        base.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
-    }
-    // Launch arguments for solve iterations i .. i + n - 1 (0-based).
-    auto iteration_launch = [&](int32_t i, int32_t n) {
-        KArgs a = base;
-        a.n_iters = n;
-        a.t = t_start + i;
-        a.iter_no = i + 1;
-        a.reduce = 1;
-        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i & 1) : 0;
-        if (defer && i > 0) {
-            a.pend_m = i;
-            a.pend_t = t_start + i - 1;
-        }
-        if (trace) {
-            if (!defer && trace->prices) a.tr_lam = trace->prices + static_cast<size_t>(i) * B * R;
-            if (!defer && trace->demand) a.tr_U = trace->demand + static_cast<size_t>(i) * B * R;
-            if (trace->choice) a.choice = trace->choice + static_cast<size_t>(i) * B * N;
-        }
-        return a;
-    };
-    for (int32_t i0 = 0; i0 < iters; i0 += kLaunchChunk) {
-        const int n = std::min<int32_t>(kLaunchChunk, iters - i0);
-        if (persistent) {
-            const KArgs a = iteration_launch(i0, n);
-            const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
-                                           : launch_dense_persistent(R, c->pl.lpj, a, B, s);
-            if (e == hipSuccess) continue;
-            (void)hipGetLastError();           // not left for the next launch's error check
-            if (!c->auto_mode) return ESP_ERR_DEVICE;
-            persistent = false;                // fall back to one launch per iteration
-            c->fell_back = true;
-        }
-        for (int i = 0; i < n; ++i)
-            if ((st = dev(launch_select(c, iteration_launch(i0 + i, 1), s))) != ESP_OK) return st;
-    }
-    // Closing launch: completes the last iteration of a deferred solve, and
-    // re-selects at the final prices (no update) when asked to.
-    KArgs a = base;
-    a.lam_out = nullptr;
-    a.tr_lam = a.tr_U = nullptr;
-    a.defer = 0;
-    a.n_iters = 1;
-    a.skip_mask = kFlagError | kFlagFrozen;
-    if (defer && iters > 0) {
-        a.pend_m = iters;
-        a.pend_t = t_start + iters - 1;
-    }
-    if (choice || demand) {
-        a.choice = choice;
-        a.demand_out = demand;
-        a.reduce = demand ? 1 : 0;
-        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(iters & 1) : 0;
-        if ((st = dev(launch_select(c, a, s))) != ESP_OK) return st;
-    } else if (a.pend_m > 0) {
-        if ((st = dev(launch_finish(R, a, B, s))) != ESP_OK) return st;
-    }
-    if (iters_done &&
-        hipMemcpyAsync(iters_done, d_iters, sizeof(int32_t) * B, hipMemcpyDeviceToDevice, s) != hipSuccess)
-        return ESP_ERR_DEVICE;
-    return ESP_OK;
+    return solve_with(c, c->base, reinterpret_cast<int32_t *>(c->ws + c->pl.o_iters), prices, iters, t_start, tol,
+                      choice, demand, trace, iters_done, stream);
+}
+
+esp_status esp_solve_noalloc(esp_ctx *c, double *prices, int32_t iters, int32_t t_start, double tol,
+                             int32_t *choice, double *demand, const esp_trace *trace, int32_t *iters_done,
+                             void *stream) {
+    esp_status st = check_ctx(c);
+    if (st != ESP_OK) return st;
+    const ScratchLayout L = scratch_layout(c->pl);
+    if (L.total > ESP_NOALLOC_SCRATCH_BYTES) return ESP_ERR_WORKSPACE;
+    if (c->scratch == nullptr) return ESP_ERR_DEVICE;
+    KArgs k = c->base;
+    k.partials = reinterpret_cast<uint64_t *>(c->scratch + L.part);
+    k.tickets = reinterpret_cast<uint32_t *>(c->scratch + L.tick);
+    k.sync = reinterpret_cast<uint32_t *>(c->scratch + L.sync);
+    k.lam_ws = reinterpret_cast<double *>(c->scratch + L.lamws);
+    k.conv_at = reinterpret_cast<int32_t *>(c->scratch + L.conv);
+    return solve_with(c, k, reinterpret_cast<int32_t *>(c->scratch + L.iters), prices, iters, t_start, tol, choice,
+                      demand, trace, iters_done, stream);
 }
 
 esp_status esp_set_penalties(esp_ctx *c, const int32_t *current, const double *switch_cost, const float *penalty,

@@ -894,6 +894,7 @@ __global__ void k_prepare(KArgs a, const double *lam, double *canon, int B) {
     }
     if (a.iters_done) {
         a.iters_done[cl] = 0;
+        a.tickets[cl] = 0u;          // 0 between launches; cleared for scratch shared between solves
         for (int i = 0; i < kSyncSlots; ++i) a.sync[(static_cast<size_t>(cl) * kSyncSlots + i) * kSyncStride] = 0u;
         a.conv_at[cl] = 0;
         for (int r = 0; r < R; ++r) {
