@@ -38,7 +38,9 @@ def _parse():
     ap.add_argument("--iters", type=int, default=0, help="override T (0 = the workload's own)")
     ap.add_argument("--blocks", type=int, default=0, help="workgroups per cluster (0 = library default)")
     ap.add_argument("--sweep", type=int, default=0, help="0 = alternate sweep direction, 1 = forward only")
-    ap.add_argument("--mode", type=int, default=0, help="loop driver: 0 auto, 1 one launch per iteration, 2 persistent")
+    ap.add_argument("--mode", type=int, default=0,
+                    help="loop driver: 0 auto, 1 one launch per iteration, 2 persistent (table streamed every "
+                         "iteration), 3 resident (tiles held in registers)")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step (price reset + esp_solve, one launch per pass) in a HIP graph and time "
                          "its replays")
@@ -49,6 +51,13 @@ def _parse():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (10 times): the reference kernel "
                          "whose FETCH_SIZE / WRITE_SIZE counters scale the fused kernel's")
+    ap.add_argument("--calibrate-stream", default="", metavar="CONFIG",
+                    help="only time the read-only streaming probe (libesp_calib.so: the fused dense kernel's load "
+                         "pattern with no work) over a table laid out like CONFIG's packed table, on the fused "
+                         "kernel's grid; prints the ceiling in GB/s")
+    ap.add_argument("--stream-mb", type=float, default=0.0,
+                    help="with --calibrate-stream: resize the table to about this many MB (memory-side cache "
+                         "check); 0 = CONFIG's size")
     ap.add_argument("--epochs", type=int, default=0, metavar="E",
                     help="instead of the default line: E scheduling epochs of an active market plus a pending "
                          "queue (C_eff of Eq. 12 each epoch, then esp_solve to tol 1e-3 from cold and from "
@@ -130,6 +139,9 @@ def main() -> int:
         print(json.dumps({"calibrate_copy_bytes": n * 4, "copies": 10}), flush=True)
         return 0
 
+    if args.calibrate_stream:
+        return _calibrate_stream(args, np, torch)
+
     import paper_2608_07971_amd as esp
     import workloads
 
@@ -187,7 +199,9 @@ def main() -> int:
     sec = ms_total / 1e3
     configs = inst.B * inst.nnz
     passes = (T + 1) * args.steps                    # T fused iterations + the final re-selection
-    persistent = solver.loop_driver() == esp.ESP_MODE_PERSISTENT and not args.graph
+    driver = solver.loop_driver()
+    persistent = driver == esp.ESP_MODE_PERSISTENT and not args.graph
+    resident = driver == esp.ESP_MODE_RESIDENT and not args.graph
     # algorithmic bytes: the fp32 table read once per iteration, plus the
     # family boundaries (one 4-byte offset per job) for ragged families
     csr = inst.dense_k is None or inst.dense_k not in (4, 8, 16, 32, 64)
@@ -228,9 +242,10 @@ def main() -> int:
                      "kernel": ("k_csr" if csr else "k_dense") + " (fused score/select/demand/update)",
                      "driver": ("graph: replays of a captured step, one launch per pass" if args.graph
                                 else "persistent: one cooperative launch runs the T passes" if persistent
-                                else "stream: one launch per pass"),
+                                else "resident: one launch runs the T passes over tiles held in registers"
+                                if resident else "stream: one launch per pass"),
                      "bytes_per_pass": bytes_per_pass, "avg_pass_us": avg_pass_s * 1e6,
-                     "passes_per_launch": T if persistent else 1},
+                     "passes_per_launch": T if (persistent or resident) else 1},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = _cpu_baseline(inst, args.cpu_seconds)
@@ -419,6 +434,59 @@ def _schedule(args, esp, workloads, np, torch) -> int:
     }
     print(json.dumps(out), flush=True)
     s.close()
+    return 0
+
+
+def _calibrate_stream(args, np, torch) -> int:
+    """Streaming ceiling of the packed-table layout: the probe kernel reads a
+    table of CONFIG's shape (its columns and tiles; dense families) with the
+    fused kernel's access pattern and grid, and nothing else."""
+    import ctypes
+
+    import workloads
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_07971_amd", "libesp_calib.so"))
+    lib.esp_calib_stream.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                                     ctypes.c_void_p, ctypes.c_void_p]
+    lib.esp_calib_stream.restype = ctypes.c_int
+    inst = workloads.make(args.calibrate_stream)
+    if inst.dense_k not in (4, 8, 16, 32, 64):
+        print("bench.py: --calibrate-stream takes a dense workload (tiny, small, large, batched)", file=sys.stderr)
+        return 2
+    ncol = 1 + inst.R
+    jobs_per_tile = 64 // (inst.dense_k // 4)
+    tiles = -(-inst.N // jobs_per_tile)
+    if args.stream_mb > 0:
+        tiles = max(1, int(round(args.stream_mb * 1e6 / (ncol * 256 * 4))))
+    col_len = (tiles + 7) * 256                            # the packer's column pad
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = args.blocks or max(1, min(3 * cus // 4, -(-tiles // 4)))
+    table = torch.ones(ncol * col_len, dtype=torch.float32, device="cuda:0")
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda:0")
+    stream = torch.cuda.Stream()
+    h = ctypes.c_void_p(stream.cuda_stream)
+
+    def launch():
+        rc = lib.esp_calib_stream(table.data_ptr(), ncol, col_len, tiles, blocks, sink.data_ptr(), h)
+        assert rc == 0, rc
+
+    passes = max(1, args.steps) * 20
+    with torch.cuda.stream(stream):
+        for _ in range(max(1, args.warmup) * 5):
+            launch()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(passes):
+            launch()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / passes
+    nbytes = tiles * 256 * ncol * 4
+    gbs = nbytes / (us * 1e-6) / 1e9
+    print(json.dumps({"calibrate_stream": args.calibrate_stream, "kernel": "k_stream_probe (libesp_calib.so)",
+                      "columns": ncol, "tiles": tiles, "blocks": blocks, "bytes_per_pass": nbytes,
+                      "passes": passes, "avg_pass_us": us, "GB/s": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS}),
+          flush=True)
     return 0
 
 

@@ -64,7 +64,8 @@ enum { ESP_STEP_CONST = 0, ESP_STEP_INV_SQRT = 1 };
 
 /* Loop drivers of esp_solve (results are identical in every mode). */
 enum {
-    ESP_MODE_AUTO = 0,        /* persistent for short passes (packed table of at most
+    ESP_MODE_AUTO = 0,        /* resident (below) when the table fits; else persistent for
+                                 short passes (packed table of at most
                                  ESP_AUTO_PERSISTENT_BYTES), where launch latency would dominate,
                                  and for solves with tol > 0 (the loop ends on the device once
                                  every cluster has converged); one launch per iteration
@@ -72,9 +73,18 @@ enum {
                                  back to one launch per iteration when the device cannot hold
                                  the grid co-resident */
     ESP_MODE_STREAM = 1,      /* one fused launch per iteration */
-    ESP_MODE_PERSISTENT = 2   /* one cooperative launch runs all iterations; the workgroups of a
-                                 cluster meet at a barrier after each iteration (ESP_ERR_DEVICE
-                                 when the grid cannot be co-resident) */
+    ESP_MODE_PERSISTENT = 2,  /* one cooperative launch runs all iterations, streaming the table
+                                 from memory every iteration; the workgroups of a cluster meet at
+                                 a barrier after each iteration (ESP_ERR_DEVICE when the grid
+                                 cannot be co-resident) */
+    ESP_MODE_RESIDENT = 3     /* one launch runs all iterations over tiles held in registers
+                                 (every wavefront of the grid holds at most two 256-entry tiles:
+                                 tables of up to about 2,000 tiles per cluster); each iteration
+                                 is completed inside the launch, the workgroups of a cluster
+                                 exchanging their exact sums through tagged words (cooperative
+                                 launch; ESP_ERR_DEVICE when the grid cannot be co-resident).
+                                 esp_create returns ESP_ERR_SHAPE when the table does not fit.
+                                 ESP_MODE_AUTO takes this driver whenever the table fits. */
 };
 
 #define ESP_AUTO_PERSISTENT_BYTES (64u << 20)
@@ -202,8 +212,8 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
  *   iters       T >= 0;  t_start >= 1 (a warm start continues a previous solve)
  * Graph capture: while `stream` is being captured, the iterations are
  * recorded as one launch each (ESP_MODE_AUTO falls back to it;
- * ESP_MODE_PERSISTENT returns ESP_ERR_INVALID_ARG); a replay recomputes the
- * same iterations on the buffers given at capture.
+ * ESP_MODE_PERSISTENT and ESP_MODE_RESIDENT return ESP_ERR_INVALID_ARG); a
+ * replay recomputes the same iterations on the buffers given at capture.
  *   tol         0 = run all T iterations; > 0 = a cluster stops after the first
  *               update with |lambda^{t+1}_r - lambda^t_r| <= tol * max(1, lambda^t_r)
  *               for every r (its later iterations do nothing)
@@ -211,11 +221,11 @@ esp_status esp_update_prices(esp_ctx *ctx, const double *demand, int32_t t, doub
  *   demand      device [B][R] or NULL: U at that selection
  *   trace       NULL or per-iteration records (see esp_trace)
  *   iters_done  device [B] int32 or NULL: updates made per cluster
- * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG (also: ESP_MODE_PERSISTENT while
- * `stream` is being captured; nothing is enqueued or recorded then),
- * ESP_ERR_DEVICE (a HIP call failed, or ESP_MODE_PERSISTENT with a grid the
- * device cannot hold co-resident: refused on the host before the first
- * iteration is launched).
+ * Errors: ESP_ERR_STATE, ESP_ERR_INVALID_ARG (also: ESP_MODE_PERSISTENT or
+ * ESP_MODE_RESIDENT while `stream` is being captured; nothing is enqueued or
+ * recorded then), ESP_ERR_DEVICE (a HIP call failed, or ESP_MODE_PERSISTENT /
+ * ESP_MODE_RESIDENT with a grid the device cannot hold co-resident: refused
+ * on the host before the first iteration is launched).
  */
 esp_status esp_solve(esp_ctx *ctx, double *prices, int32_t iters, int32_t t_start, double tol,
                      int32_t *choice, double *demand, const esp_trace *trace, int32_t *iters_done,
@@ -401,9 +411,9 @@ esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_
 
 /*
  * esp_loop_driver: the loop driver esp_solve uses for this context's solves
- * with tol = 0, ESP_MODE_STREAM or ESP_MODE_PERSISTENT (ESP_MODE_AUTO
- * resolved against the table size, and against the device once a solve has
- * run).  Host-only.
+ * with tol = 0, ESP_MODE_STREAM, ESP_MODE_PERSISTENT or ESP_MODE_RESIDENT
+ * (ESP_MODE_AUTO resolved against the table size, and against the device
+ * once a solve has run).  Host-only.
  * Errors: ESP_ERR_STATE (NULL context), ESP_ERR_INVALID_ARG (mode NULL).
  */
 esp_status esp_loop_driver(const esp_ctx *ctx, int32_t *mode);

@@ -35,6 +35,7 @@ ESP_STEP_INV_SQRT = 1
 ESP_MODE_AUTO = 0
 ESP_MODE_STREAM = 1
 ESP_MODE_PERSISTENT = 2
+ESP_MODE_RESIDENT = 3
 ESP_OPT_PROFILE_STORE = 1
 
 

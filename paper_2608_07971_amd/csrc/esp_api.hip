@@ -43,7 +43,7 @@ struct Plan {
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
            o_tick = 0, o_flags = 0, o_iters = 0, o_sync = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
-           o_aos = 0, o_lamws = 0, o_conv = 0, total = 0;
+           o_aos = 0, o_lamws = 0, o_conv = 0, o_xch = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -90,7 +90,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     if (opt) {
         if (opt->blocks_per_cluster < 0) return ESP_ERR_INVALID_ARG;
         if (opt->sweep_order != 0 && opt->sweep_order != 1) return ESP_ERR_INVALID_ARG;
-        if (opt->mode < ESP_MODE_AUTO || opt->mode > ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
+        if (opt->mode < ESP_MODE_AUTO || opt->mode > ESP_MODE_RESIDENT) return ESP_ERR_INVALID_ARG;
         if ((opt->flags & ~ESP_OPT_PROFILE_STORE) != 0) return ESP_ERR_INVALID_ARG;
         for (int i = 0; i < 4; ++i)
             if (opt->reserved[i] != 0) return ESP_ERR_INVALID_ARG;
@@ -171,6 +171,7 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_aos = o;   o = align_up(o + B * static_cast<size_t>(pl->nnz) * pl->aos_stride * sizeof(float));
     pl->o_lamws = o; o = align_up(o + 2 * B * R * sizeof(double));
     pl->o_conv = o;  o = align_up(o + B * sizeof(int32_t));
+    pl->o_xch = o;   o = align_up(o + 2 * B * pl->nblk * R * kMaxLimbs * sizeof(uint64_t));
     pl->total = o;
     return ESP_OK;
 }
@@ -230,7 +231,7 @@ char *resolve_scratch(int dev) {
 // Byte offsets of the per-solve scratch regions of a plan inside the static
 // array, each 256-byte aligned; the last value is the size.
 struct ScratchLayout {
-    size_t part = 0, tick = 0, iters = 0, sync = 0, lamws = 0, conv = 0, total = 0;
+    size_t part = 0, tick = 0, iters = 0, sync = 0, lamws = 0, conv = 0, xch = 0, total = 0;
 };
 
 ScratchLayout scratch_layout(const Plan &pl) {
@@ -243,6 +244,7 @@ ScratchLayout scratch_layout(const Plan &pl) {
     L.sync = o;  o = align_up(o + B * kSyncSlots * kSyncStride * sizeof(uint32_t));
     L.lamws = o; o = align_up(o + 2 * B * R * sizeof(double));
     L.conv = o;  o = align_up(o + B * sizeof(int32_t));
+    L.xch = o;   o = align_up(o + 2 * B * pl.nblk * R * kMaxLimbs * sizeof(uint64_t));
     L.total = o;
     return L;
 }
@@ -263,6 +265,7 @@ struct esp_ctx {
     int mode = ESP_MODE_AUTO;
     bool auto_mode = false;            // the caller asked for ESP_MODE_AUTO
     bool fell_back = false;            // AUTO: the device refused a co-resident grid
+    bool resident_ok = false;          // persistent solves may hold the tiles in registers
     std::vector<int64_t> off;          // family offsets (host copy)
     std::vector<int64_t> slot_of;      // first table slot of each family
     KArgs base{};
@@ -358,37 +361,54 @@ esp_status solve_with(esp_ctx *c, const KArgs &kb, int32_t *d_iters, double *pri
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     if (hipStreamIsCapturing(s, &cap) != hipSuccess) return ESP_ERR_DEVICE;
     const bool capturing = cap != hipStreamCaptureStatusNone;
-    if (capturing && c->mode == ESP_MODE_PERSISTENT) return ESP_ERR_INVALID_ARG;
-    {
-        // validates the prices, turns -0.0 into +0.0 in place, resets the
-        // per-solve state
-        KArgs p = kb;
-        p.iters_done = d_iters;
-        if ((st = dev(launch_prepare(R, p, prices, prices, B, s))) != ESP_OK) return st;
-    }
-    // With several workgroups per cluster every iteration only publishes its
-    // sums; the next launch (or the closing one) completes it.  With one
-    // workgroup per cluster the workgroup completes its own iteration.
-    const bool defer = c->pl.nblk > 1;
+    if (capturing && (c->mode == ESP_MODE_PERSISTENT || c->mode == ESP_MODE_RESIDENT)) return ESP_ERR_INVALID_ARG;
+    // The loop driver: persistent launches (one per chunk of up to
+    // kLaunchChunk iterations) or one launch per iteration.  Persistent
+    // launches run over register-resident tiles when every wavefront of the
+    // grid holds at most two tiles (tables of up to a few MB, where the
+    // latency of an iteration, not the bandwidth, sets the pace): each launch
+    // then completes all of its iterations itself.
     bool persistent =
         !capturing && !c->fell_back && (c->mode != ESP_MODE_STREAM || (c->auto_mode && tol > 0.0));
-    KArgs base = kb;
-    base.lam_in = prices;
-    base.lam_dst = prices;
-    base.iters_done = d_iters;
-    base.tol = tol;
-    base.defer = defer ? 1 : 0;
-    if (defer) {
-        base.lam_out = nullptr;
-        base.skip_mask = kFlagError | kFlagFrozen;
-        if (trace) {
-            base.trace_lam = trace->prices;
-            base.trace_U = trace->demand;
-        }
-    } else {
-        base.lam_out = prices;
-        base.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
+    bool resident = persistent && (c->mode == ESP_MODE_RESIDENT || (c->auto_mode && c->resident_ok));
+    {
+        // validates the prices, turns -0.0 into +0.0 in place, resets the
+        // per-solve state (and the exchange words of a resident solve)
+        KArgs p = kb;
+        p.iters_done = d_iters;
+        p.xch_clear = (resident && c->pl.nblk > 1)
+                          ? 2 * static_cast<size_t>(B) * c->pl.nblk * static_cast<size_t>(kb.xch_stride) : 0;
+        if ((st = dev(launch_prepare(R, p, prices, prices, B, s))) != ESP_OK) return st;
     }
+    // With several workgroups per cluster and no resident launch, every
+    // iteration only publishes its sums; the next launch (or the closing
+    // one) completes it.  With one workgroup per cluster, or in a resident
+    // launch, the iteration is completed where it runs.
+    bool defer = false;
+    KArgs base;
+    auto setup = [&]() {
+        defer = !resident && c->pl.nblk > 1;
+        base = kb;
+        base.lam_in = prices;
+        base.lam_dst = prices;
+        base.iters_done = d_iters;
+        base.tol = tol;
+        base.defer = defer ? 1 : 0;
+        base.xch_clear = 0;
+        if (defer) {
+            base.lam_out = nullptr;
+            base.skip_mask = kFlagError | kFlagFrozen;
+            if (trace) {
+                base.trace_lam = trace->prices;
+                base.trace_U = trace->demand;
+            }
+        } else {
+            base.lam_out = prices;
+            base.skip_mask = kFlagError | kFlagStopped | kFlagFrozen;
+        }
+        if (resident) base.sweep_alt = 0;      // a wavefront keeps the same tiles
+    };
+    setup();
     // Launch arguments for solve iterations i .. i + n - 1 (0-based).
     auto iteration_launch = [&](int32_t i, int32_t n) {
         KArgs a = base;
@@ -396,7 +416,7 @@ esp_status solve_with(esp_ctx *c, const KArgs &kb, int32_t *d_iters, double *pri
         a.t = t_start + i;
         a.iter_no = i + 1;
         a.reduce = 1;
-        a.reverse = (c->sweep == 0) ? static_cast<int32_t>(i & 1) : 0;
+        a.reverse = (c->sweep == 0 && !resident) ? static_cast<int32_t>(i & 1) : 0;
         if (defer && i > 0) {
             a.pend_m = i;
             a.pend_t = t_start + i - 1;
@@ -412,13 +432,24 @@ esp_status solve_with(esp_ctx *c, const KArgs &kb, int32_t *d_iters, double *pri
         const int n = std::min<int32_t>(kLaunchChunk, iters - i0);
         if (persistent) {
             const KArgs a = iteration_launch(i0, n);
-            const hipError_t e = c->pl.csr ? launch_csr_persistent(R, a, B, s)
-                                           : launch_dense_persistent(R, c->pl.lpj, a, B, s);
+            hipError_t e;
+            if (resident)
+                e = c->pl.csr ? launch_csr_resident(R, a, B, s) : launch_dense_resident(R, c->pl.lpj, a, B, s);
+            else
+                e = c->pl.csr ? launch_csr_persistent(R, a, B, s) : launch_dense_persistent(R, c->pl.lpj, a, B, s);
             if (e == hipSuccess) continue;
             (void)hipGetLastError();           // not left for the next launch's error check
-            if (!c->auto_mode) return ESP_ERR_DEVICE;
-            persistent = false;                // fall back to one launch per iteration
+            // A refused grid enqueues nothing.  AUTO falls back to one launch
+            // per iteration: from here on for deferred persistent launches
+            // (same completion scheme), from the first iteration for resident
+            // ones (which can only be refused at their first launch).
+            if (!c->auto_mode || (resident && i0 > 0)) return ESP_ERR_DEVICE;
+            persistent = false;
             c->fell_back = true;
+            if (resident) {
+                resident = false;
+                setup();
+            }
         }
         for (int i = 0; i < n; ++i)
             if ((st = dev(launch_select(c, iteration_launch(i0 + i, 1), s))) != ESP_OK) return st;
@@ -551,6 +582,20 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
             need_bits = std::max(need_bits, hi - lo + lgN);
             shift[static_cast<size_t>(b) * R + r] = lo;
         }
+
+    // Resident persistent launches (ESP_MODE_RESIDENT): every wavefront of
+    // the grid holds at most two tiles, and with several workgroups per
+    // cluster each thread reads at most kXchPerThread exchange words (sums in
+    // 48-bit limbs) per round.
+    const int limbs = std::max(1, (need_bits + 47) / 48);
+    bool resident_ok = false;
+    {
+        const int64_t waves = static_cast<int64_t>(pl.nblk) * kBlockWaves;
+        const int groups = kBlockThreads / (R * limbs);
+        resident_ok = static_cast<int64_t>(pl.tiles) <= 2 * waves &&
+                      (pl.nblk == 1 || (groups >= 1 && pl.nblk <= kXchPerThread * groups));
+    }
+    if (options && options->mode == ESP_MODE_RESIDENT && !resident_ok) return ESP_ERR_SHAPE;
 
     // ---- workspace ----
     if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0 || workspace_bytes < pl.total)
@@ -757,6 +802,11 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     k.lam_ws = reinterpret_cast<double *>(ws + pl.o_lamws);
     k.conv_at = reinterpret_cast<int32_t *>(ws + pl.o_conv);
     k.sweep_alt = c->sweep == 0 ? 1 : 0;
+    k.limbs = limbs;
+    k.xch_stride = R * limbs;
+    k.xch = reinterpret_cast<uint64_t *>(ws + pl.o_xch);
+    k.xch_clear = 0;
+    c->resident_ok = resident_ok;
     *out = c;
     return ESP_OK;
 }
@@ -824,6 +874,7 @@ esp_status esp_solve_noalloc(esp_ctx *c, double *prices, int32_t iters, int32_t 
     k.sync = reinterpret_cast<uint32_t *>(c->scratch + L.sync);
     k.lam_ws = reinterpret_cast<double *>(c->scratch + L.lamws);
     k.conv_at = reinterpret_cast<int32_t *>(c->scratch + L.conv);
+    k.xch = reinterpret_cast<uint64_t *>(c->scratch + L.xch);
     return solve_with(c, k, reinterpret_cast<int32_t *>(c->scratch + L.iters), prices, iters, t_start, tol, choice,
                       demand, trace, iters_done, stream);
 }
@@ -1045,7 +1096,9 @@ esp_status esp_loop_driver(const esp_ctx *c, int32_t *mode) {
     esp_status st = check_ctx(c);
     if (st != ESP_OK) return st;
     if (mode == nullptr) return ESP_ERR_INVALID_ARG;
-    *mode = (c->mode == ESP_MODE_STREAM || c->fell_back) ? ESP_MODE_STREAM : ESP_MODE_PERSISTENT;
+    if (c->mode == ESP_MODE_STREAM || c->fell_back) *mode = ESP_MODE_STREAM;
+    else if (c->mode == ESP_MODE_RESIDENT || (c->auto_mode && c->resident_ok)) *mode = ESP_MODE_RESIDENT;
+    else *mode = ESP_MODE_PERSISTENT;
     return ESP_OK;
 }
 

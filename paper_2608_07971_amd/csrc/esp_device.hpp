@@ -118,6 +118,32 @@ __device__ __forceinline__ uint64_t *partials_of(const KArgs &a, int k, int cl) 
 // atomic exchanges, which are performed at the device coherence point, and
 // wait until they have completed (their old values are back).  Runs in
 // wavefront 0; the caller orders the rest of the workgroup.
+//
+// Why a reader elsewhere on the device then sees these sums (the argument
+// for publish_sums / cluster_sums here and for the persistent barrier of the
+// kernels; it rests on how gfx950 performs agent-scope atomics, not on a
+// release/acquire pair, whose cache-wide writeback and invalidation cost
+// 12 us per iteration at 256 workgroups):
+//  1. The 8 XCDs each have their own L2, which is not coherent with the
+//     others.  Agent-scope atomic operations are not performed in an XCD's
+//     L2: they travel to the memory-side coherence point of their address
+//     (shared by all XCDs), and one that returns a value returns it only
+//     after it has been performed there.  Agent-scope atomic loads read from
+//     that point as well, never from a stale L2 line.
+//  2. s_waitcnt vmcnt(0) on the returned values therefore means every
+//     exchange below has been performed at the coherence point before the
+//     workgroup issues anything after it: the ticket or arrival add that
+//     signals "published" is issued later, so it is performed later.
+//  3. A reader learns "all published" from the value another atomic
+//     returned (the last ticket, or a release word stored only after the
+//     last arrival add had returned), and issues its loads of the sums only
+//     after that value is back (the loads depend on it).  They are performed
+//     after every exchange was, at the same point, so they return the
+//     published sums.
+// What would break it: workgroup scope (performed in one XCD's L2), plain
+// stores (held in the writer's L2 until evicted), plain loads (a stale line
+// in the reader's L2), a non-returning add or a missing wait (the signal
+// could overtake the sums on their way to the coherence point).
 template <int R>
 __device__ __forceinline__ void publish_sums(const KArgs &a, int k, int cl, int blk, const u128 *bsum) {
     const int t = threadIdx.x;

@@ -28,6 +28,11 @@ constexpr int kSyncStride = 64;                     // uint32 words between barr
 // iteration parity (deferred completion), 2 those of in-launch completion.
 constexpr int kPartialBuffers = 3;
 constexpr int kInLaunchBuffer = 2;
+// Resident launches with several workgroups per cluster exchange their sums
+// as limbs of 48 bits (at most 3 for 127-bit sums) in tagged 64-bit words;
+// each thread of a workgroup reads at most kXchPerThread words per round.
+constexpr int kMaxLimbs = 3;
+constexpr int kXchPerThread = 8;
 
 // Flags per cluster (device int32).
 constexpr int kFlagStopped = 1;                     // converged under tol: skip further updates
@@ -117,6 +122,12 @@ struct KArgs {
     int32_t *conv_at;              // [B] iteration whose completion met tol, 0 while none has
     double *trace_lam;             // [iters][B][R]: row m - 1 receives lambda_{m+1}, or NULL
     double *trace_U;               // [iters][B][R]: row m - 1 receives U_m, or NULL
+    // Resident launches (tiles held in registers, every iteration completed
+    // in the launch): tagged exchange words [2][B][nblk][xch_stride].
+    uint64_t *xch;
+    int32_t xch_stride;            // words per workgroup = R * limbs
+    int32_t limbs;                 // 48-bit limbs per workgroup sum
+    size_t xch_clear;              // words k_prepare sets to 0 before a resident solve (0: none)
 };
 
 constexpr int kStatusTimeout = 8;  // a persistent wait exceeded its bound
@@ -129,6 +140,10 @@ hipError_t launch_dense(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_dense_persistent(int R, int lpj, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_csr_persistent(int R, const KArgs &a, int B, hipStream_t s);
+// Multi-iteration launches over register-resident tiles (at most two per
+// wavefront), each iteration completed in the launch (see kResident).
+hipError_t launch_dense_resident(int R, int lpj, const KArgs &a, int B, hipStream_t s);
+hipError_t launch_csr_resident(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_gather(int R, const KArgs &a, int B, hipStream_t s);
 hipError_t launch_update(int R, const KArgs &a, const double *demand_in, int B, hipStream_t s);
 // Validates prices `lam`; `canon` (NULL or the same buffer, writable) receives

@@ -187,3 +187,22 @@ def test_workspace_grows_by_one_column_with_penalties():
     b = workloads.with_penalties(workloads.random_small(10, 50, 8, 3, dense=True), 10)
     na, nb = _ws(esp.Problem.from_instance(a)), _ws(esp.Problem.from_instance(b))
     assert nb - na >= 50 * 8 * 4
+
+
+def test_resident_mode_refuses_tables_that_do_not_fit():
+    """ESP_MODE_RESIDENT needs every wavefront to hold at most two tiles:
+    refused with ESP_ERR_SHAPE before any device work (here: no workspace at
+    all); a table that fits gets as far as the workspace check."""
+    def create(inst, blocks):
+        p = esp.Problem.from_instance(inst)
+        e0 = np.ascontiguousarray(inst.eta0, dtype=np.float64)
+        step = esp.esp_step_rule(inst.rule, e0.ctypes.data)
+        opt = esp.esp_options(blocks, 0, esp.ESP_MODE_RESIDENT, 0)
+        out = C.c_void_p(None)
+        return esp.lib().esp_create(C.addressof(p.c), C.addressof(step), C.addressof(opt), None, 0, None,
+                                    C.byref(out))
+    small = workloads.make("small", n_jobs=200)          # 25 tiles
+    assert create(small, 3) == esp.ESP_ERR_SHAPE          # 12 wavefronts hold at most 24
+    assert create(small, 4) == esp.ESP_ERR_WORKSPACE
+    assert create(workloads.make("tiny"), 0) == esp.ESP_ERR_WORKSPACE
+    assert create(workloads.make("large", n_jobs=100000), 0) == esp.ESP_ERR_SHAPE

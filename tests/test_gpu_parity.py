@@ -124,12 +124,14 @@ def test_run_to_run_and_geometry_determinism():
 
 
 def test_auto_driver_follows_table_size():
-    """AUTO runs the persistent driver for short passes and one launch per
-    pass for large tables; explicit modes are kept."""
-    _say("auto driver tiny/large")
-    for name, want in (("tiny", esp.ESP_MODE_PERSISTENT), ("small", esp.ESP_MODE_PERSISTENT),
-                       ("large", esp.ESP_MODE_STREAM)):
-        s = esp.Solver(workloads.make(name))
+    """AUTO runs the resident driver for tables whose tiles fit the grid's
+    registers, the persistent driver for other short passes and one launch
+    per pass for large tables; explicit modes are kept."""
+    _say("auto driver tiny/small/large")
+    for name, kw, want in (("tiny", {}, esp.ESP_MODE_RESIDENT), ("small", {}, esp.ESP_MODE_RESIDENT),
+                           ("large", {"n_jobs": 20000}, esp.ESP_MODE_PERSISTENT),
+                           ("large", {}, esp.ESP_MODE_STREAM)):
+        s = esp.Solver(workloads.make(name, **kw))
         assert s.loop_driver() == want, name
         s.close()
     s = esp.Solver(workloads.make("tiny"), mode=esp.ESP_MODE_STREAM)
