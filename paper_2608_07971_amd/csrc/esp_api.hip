@@ -585,15 +585,16 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
 
     // Resident persistent launches (ESP_MODE_RESIDENT): every wavefront of
     // the grid holds at most two tiles, and with several workgroups per
-    // cluster each thread reads at most kXchPerThread exchange words (sums in
-    // 48-bit limbs) per round.
+    // cluster each lane reads at most kXchPerThread exchange words (sums in
+    // 48-bit limbs) per round: wavefront w of a workgroup reads workgroups
+    // w, w + 4, ..., with 64 / (R limbs) lanes per limb position.
     const int limbs = std::max(1, (need_bits + 47) / 48);
     bool resident_ok = false;
     {
         const int64_t waves = static_cast<int64_t>(pl.nblk) * kBlockWaves;
-        const int groups = kBlockThreads / (R * limbs);
+        const int groups = kWaveSize / (R * limbs);
         resident_ok = static_cast<int64_t>(pl.tiles) <= 2 * waves &&
-                      (pl.nblk == 1 || (groups >= 1 && pl.nblk <= kXchPerThread * groups));
+                      (pl.nblk == 1 || (groups >= 1 && pl.nblk <= kXchPerThread * kBlockWaves * groups));
     }
     if (options && options->mode == ESP_MODE_RESIDENT && !resident_ok) return ESP_ERR_SHAPE;
 

@@ -108,6 +108,20 @@ __device__ __forceinline__ double fx_to_double(u128 a, int sh) {
     return ldexp(static_cast<double>(m), drop + sh);
 }
 
+// The same for a 64-bit accumulator (fewer instructions where the sums are
+// known to fit 64 bits).
+__device__ __forceinline__ double fx_to_double(uint64_t a, int sh) {
+    if (a == 0) return 0.0;
+    const int h = 63 - __clzll(a);
+    if (h <= 52) return ldexp(static_cast<double>(a), sh);
+    const int drop = h - 52;
+    uint64_t m = a >> drop;
+    const uint64_t rem = a & ((1ull << drop) - 1);
+    const uint64_t half = 1ull << (drop - 1);
+    if (rem > half || (rem == half && (m & 1u))) m += 1;   // m <= 2^53: exact as a double
+    return ldexp(static_cast<double>(m), drop + sh);
+}
+
 // Partial-sum buffer k of cluster cl: [nblk][R][2] 64-bit words (low, high).
 template <int R>
 __device__ __forceinline__ uint64_t *partials_of(const KArgs &a, int k, int cl) {

@@ -321,92 +321,161 @@ __device__ __forceinline__ uint64_t *xch_words(const KArgs &a, int cl, int m) {
     return a.xch + (static_cast<size_t>(m & 1) * a.B + cl) * static_cast<size_t>(a.nblk) * a.xch_stride;
 }
 
-// Publish this workgroup's sums bsum[r] (LDS) for iteration a.iter_no, read
-// every workgroup's words (polling until their tags match, bounded by about
-// 2 s of the real-time counter), total them, and complete the iteration:
-// U (exact), lambda_{m+1} of Eq. 8 into lam_next (LDS) and the stop test;
-// workgroup 0 writes the prices, trace rows, update count and stop flag.
+__device__ __forceinline__ double readlane_d(double v, int lane) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<unsigned>(b)), lane);
+    const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), lane);
+    return __longlong_as_double(static_cast<long long>(
+        (static_cast<unsigned long long>(static_cast<unsigned>(hi)) << 32) | static_cast<unsigned>(lo)));
+}
+
+// Step sizes eta_t of all iterations of a resident launch, computed once at
+// its start by the whole workgroup (the same IEEE operations as step_size, so
+// the same bits), so that no division or square root lies on an iteration's
+// path.  The caller synchronizes the workgroup before the first read.
+__device__ __forceinline__ const double *resident_etas(const KArgs &a, int cl) {
+    __shared__ double s_eta[kLaunchChunk];
+    for (int i = threadIdx.x; i < a.n_iters; i += kBlockThreads) s_eta[i] = step_size(a, cl, a.t + i);
+    return s_eta;
+}
+
+// End of iteration a.iter_no in a resident launch.  `acc` is this lane's
+// exact partial sum for resource lane % R (acc_lane: the lane accumulates);
+// lam holds the iteration's prices and receives lambda_{m+1}.  Every
+// wavefront completes the iteration itself, with one workgroup barrier (two
+// when the workgroups of a cluster exchange their sums):
+//  1. each wavefront totals its lanes' sums per resource through LDS (lanes
+//     r < R hold them) and posts them; after the barrier every wavefront adds
+//     the four wavefronts' sums;
+//  2. with several workgroups per cluster, wavefront 0 publishes the
+//     workgroup's sums as tagged limbs and all four wavefronts read every
+//     workgroup's words (wavefront w the workgroups w, w + 4, ...; each lane
+//     one limb position of up to kXchPerThread workgroups, its loads in
+//     flight together, polling until every tag matches, bounded by about 2 s
+//     of the real-time counter); after a second barrier every wavefront adds
+//     the four partial totals;
+//  3. lanes r < R compute U_r (exact total rounded once), lambda_r of Eq. 8
+//     and the stop test, and the new prices reach every lane by readlane, in
+//     the same bits in every wavefront and workgroup; wavefront 0 of
+//     workgroup 0 writes the prices, trace rows, update count and stop flag.
 // Returns false when the cluster stops here or a wait timed out.
-template <int R>
-__device__ bool exchange_iteration(const KArgs &a, int cl, int blk, const u128 *bsum, const double *lam_cur,
-                                   double *lam_next, int *s_go) {
-    __shared__ unsigned long long s_tot[R * kMaxLimbs];
-    __shared__ int s_ok[R];
-    const int t = threadIdx.x;
-    const int L = a.limbs;
-    const int RL = R * L;
+template <int R, typename A>
+__device__ bool resident_complete(const KArgs &a, int cl, int blk, int wave, int lane, A acc, bool acc_lane,
+                                  double eta, double (&lam)[R]) {
+    constexpr int Q = kWaveSize / R;
+    __shared__ A s_lane[kBlockWaves][kWaveSize];
+    __shared__ A s_wave[2][kBlockWaves][R];
+    __shared__ unsigned long long s_limb[kBlockWaves][kWaveSize];
+    __shared__ unsigned long long s_xw[2][kBlockWaves][R * kMaxLimbs];
+    __shared__ int s_go;
     const int m = a.iter_no;
-    const uint64_t tag = static_cast<uint64_t>((m - 1) % 65535 + 1);
-    uint64_t *w = xch_words(a, cl, m);
-    if (t < RL) {
-        const int r = t / L, l = t - r * L;
-        const uint64_t v = static_cast<uint64_t>(bsum[r] >> (kLimbBits * l)) & kLimbMask;
-        __hip_atomic_store(w + static_cast<size_t>(blk) * a.xch_stride + t, (tag << kLimbBits) | v,
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (t < R * kMaxLimbs) s_tot[t] = 0ull;
-    if (t == 0) *s_go = 1;
-    __syncthreads();
-    // Thread (g, q), q < RL, takes the words q of workgroups g, g + G, ...
-    // (at most kXchPerThread of them, host-checked); all of its loads are in
-    // flight at once, and the round repeats until every tag matches.
-    const int G = kBlockThreads / RL;
-    const int g = t / RL, q = t - g * RL;
-    if (g < G) {
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        uint64_t sum = 0;
-        while (true) {
-            bool all = true;
-            sum = 0;
+    const int par = m & 1;
+    // 1. wavefront sums per resource
+    s_lane[wave][lane] = acc_lane ? acc : A(0);
+    wave_sync();
+    // (every partial sum fits the accumulator type A: the packer sized A for
+    // the whole column's total)
+    if (lane < R) {
+        A ws = 0;
 #pragma unroll
-            for (int u = 0; u < kXchPerThread; ++u) {
-                const int b = g + u * G;
-                const int bc = b < a.nblk ? b : a.nblk - 1;          // clamped: no branch around the load
-                const uint64_t x = __hip_atomic_load(w + static_cast<size_t>(bc) * a.xch_stride + q,
-                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const bool valid = b < a.nblk;
-                all &= !valid | ((x >> kLimbBits) == tag);
-                sum += valid ? (x & kLimbMask) : 0ull;
-            }
-            if (all) break;
-            if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
-                __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
-                atomicCAS(a.status, 0, kStatusTimeout);
-                *s_go = 0;
-                break;
+        for (int q = 0; q < Q; ++q) ws += s_lane[wave][q * R + lane];
+        s_wave[par][wave][lane] = ws;
+    }
+    if (threadIdx.x == 0) s_go = 1;
+    __syncthreads();
+    A tot = 0;
+    if (lane < R) {
+#pragma unroll
+        for (int w = 0; w < kBlockWaves; ++w) tot += s_wave[par][w][lane];
+    }
+    if (a.nblk > 1) {
+        // 2. the exchange between the workgroups of the cluster
+        const int L = a.limbs;
+        const int RL = R * L;
+        const uint64_t tag = static_cast<uint64_t>((m - 1) % 65535 + 1);
+        uint64_t *words = xch_words(a, cl, m);
+        if (wave == 0 && lane < R) {
+            for (int l = 0; l < L; ++l) {
+                const uint64_t v = static_cast<uint64_t>(static_cast<u128>(tot) >> (kLimbBits * l)) & kLimbMask;
+                __hip_atomic_store(words + static_cast<size_t>(blk) * a.xch_stride + lane * L + l,
+                                   (tag << kLimbBits) | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        atomicAdd(&s_tot[q], static_cast<unsigned long long>(sum));   // integer: any order
+        const int G = kWaveSize / RL;                 // lane groups per wavefront
+        const int g = lane / RL, q = lane - g * RL;
+        unsigned long long sum = 0;
+        if (g < G) {
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            while (true) {
+                bool all = true;
+                sum = 0;
+#pragma unroll
+                for (int u = 0; u < kXchPerThread; ++u) {
+                    const int b = wave + kBlockWaves * (g + G * u);
+                    const int bc = b < a.nblk ? b : a.nblk - 1;          // clamped: no branch around the load
+                    const uint64_t x = __hip_atomic_load(words + static_cast<size_t>(bc) * a.xch_stride + q,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const bool valid = b < a.nblk;
+                    all &= !valid | ((x >> kLimbBits) == tag);
+                    sum += valid ? (x & kLimbMask) : 0ull;
+                }
+                if (all) break;
+                if (__hip_atomic_load(a.status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+                    __builtin_amdgcn_s_memrealtime() - t0 > 200000000ull) {
+                    atomicCAS(a.status, 0, kStatusTimeout);
+                    s_go = 0;                          // every wavefront still reaches the barrier
+                    break;
+                }
+            }
+        }
+        s_limb[wave][lane] = sum;
+        wave_sync();
+        if (lane < RL) {
+            unsigned long long ps = 0;
+            for (int gg = 0; gg < G; ++gg) ps += s_limb[wave][gg * RL + lane];
+            s_xw[par][wave][lane] = ps;
+        }
+        __syncthreads();
+        if (s_go == 0) return false;
+        tot = 0;
+        if (lane < R) {
+            u128 t128 = 0;
+            for (int l = 0; l < L; ++l) {
+                u128 ls = 0;
+#pragma unroll
+                for (int w = 0; w < kBlockWaves; ++w) ls += s_xw[par][w][lane * L + l];
+                t128 += ls << (kLimbBits * l);
+            }
+            tot = static_cast<A>(t128);          // the exact total, which fits A
+        }
     }
-    __syncthreads();
-    if (*s_go == 0) return false;
-    if (t < R) {
-        u128 tot = 0;
-        for (int l = 0; l < L; ++l) tot += static_cast<u128>(s_tot[t * L + l]) << (kLimbBits * l);
-        const size_t i = static_cast<size_t>(cl) * R + t;
-        const double U = fx_to_double(tot, a.shift[i]);
-        const double lo = lam_cur[t];
+    // 3. U, Eq. 8 and the stop test in lanes r < R
+    double lo = lam[0];
+#pragma unroll
+    for (int r = 1; r < R; ++r) lo = (lane == r) ? lam[r] : lo;
+    double U = 0.0, ln = 0.0;
+    bool ok = true;
+    if (lane < R) {
+        const size_t i = static_cast<size_t>(cl) * R + lane;
+        U = fx_to_double(tot, a.shift[i]);
         const double gd = U - a.cap[i];
-        const double x = lo + step_size(a, cl, a.t) * gd;
-        const double ln = (x > 0.0) ? x : 0.0;
-        lam_next[t] = ln;
+        const double x = lo + eta * gd;
+        ln = (x > 0.0) ? x : 0.0;
         const double scale = lo > 1.0 ? lo : 1.0;
-        s_ok[t] = fabs(ln - lo) <= a.tol * scale;
-        if (blk == 0) {
+        ok = fabs(ln - lo) <= a.tol * scale;
+        if (wave == 0 && blk == 0) {
             a.lam_out[i] = ln;
             if (a.tr_lam) a.tr_lam[i] = ln;
             if (a.tr_U) a.tr_U[i] = U;
         }
     }
-    __syncthreads();
-    int all = 1;
-#pragma unroll
-    for (int r = 0; r < R; ++r) all &= s_ok[r];
-    const bool stop = a.tol > 0.0 && all;
-    if (blk == 0 && t == 0) {
+    const bool stop = (a.tol > 0.0) & (__ballot(!ok) == 0);      // wave-uniform, the same in every wavefront
+    if (wave == 0 && blk == 0 && lane == 0) {
         if (a.iters_done) a.iters_done[cl] = m;
         if (stop) atomicOr(&a.flags[cl], kFlagStopped);
     }
+#pragma unroll
+    for (int r = 0; r < R; ++r) lam[r] = readlane_d(ln, r);
     return !stop;
 }
 
@@ -567,6 +636,8 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
     if constexpr (Mode != kResident) pending_loads<R, A>(a, cl, conv, pend);   // issued first: they return first
     prefetch_two(a.reverse);                   // in flight during a pending completion; a resident
                                                // launch's tiles for all its iterations
+    const double *etas = nullptr;
+    if constexpr (Mode == kResident) etas = resident_etas(a, cl);   // read after launch_prices' barrier
     if (!launch_prices<R, A>(a, cl, blk, pend, s_lam, s_newlam, s_acc)) return;
 #pragma unroll
     for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
@@ -592,6 +663,12 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             }
         }
         if (!ai.reduce) return;
+        if constexpr (Mode == kResident) {
+            const bool go = resident_complete<R, A>(ai, cl, blk, wave, lane, acc, acc_lane, etas[it], lam);
+            acc = 0;
+            if (!go || it + 1 == a.n_iters) break;
+            continue;
+        }
 
         // Workgroup sum per resource (integer adds: any order gives the same value).
         s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
@@ -612,18 +689,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_dense(KArgs a) {
             s_bsum[threadIdx.x] = v;
         }
         __syncthreads();
-        if constexpr (Mode == kResident) {
-            if (a.nblk == 1) {
-                finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
-                if (it + 1 == a.n_iters) break;
-                if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
-            } else {
-                if (!exchange_iteration<R>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_go)) break;
-                if (it + 1 == a.n_iters) break;
-                if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
-                __syncthreads();
-            }
-        } else if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
+        if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
             publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
             prefetch_two(rev ^ a.sweep_alt);
@@ -698,9 +764,11 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
 
 // Two wavefronts per SIMD at least (at most 256 registers): the CSR grid holds
 // two workgroups per CU, and a cooperative launch needs them all resident
-// (the persistent instances at R = 8 would otherwise take a few more).
+// (the persistent instances at R = 8 would otherwise take a few more).  The
+// resident instance keeps two tiles live through every iteration and runs
+// one workgroup per CU at most: it may use the whole register file.
 template <int R, typename A, int Mode>
-__global__ __launch_bounds__(kBlockThreads, 2) void k_csr(KArgs a) {
+__global__ __launch_bounds__(kBlockThreads, Mode == kResident ? 1 : 2) void k_csr(KArgs a) {
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
     __shared__ uint32_t s_win[kBlockWaves][8];
     __shared__ float s_stage[kBlockWaves][kTileEntries][R];
@@ -880,6 +948,8 @@ __global__ __launch_bounds__(kBlockThreads, 2) void k_csr(KArgs a) {
     load_tile(min(tile0, last), a.reverse, nu, nd, npn, nhw);   // in flight during a pending completion (clamped: no branch)
     if constexpr (Mode == kResident)
         load_tile(min(tile0 + stride, last), a.reverse, bu, bd, bpn, bhw);   // the launch's second tile
+    const double *etas = nullptr;
+    if constexpr (Mode == kResident) etas = resident_etas(a, cl);   // read after launch_prices' barrier
     if (!launch_prices<R, A>(a, cl, blk, pend, s_lam, s_newlam, s_acc)) return;
 #pragma unroll
     for (int r = 0; r < R; ++r) lam[r] = s_lam[r];
@@ -900,6 +970,12 @@ __global__ __launch_bounds__(kBlockThreads, 2) void k_csr(KArgs a) {
             }
         }
         if (!ai.reduce) return;
+        if constexpr (Mode == kResident) {
+            const bool go = resident_complete<R, A>(ai, cl, blk, wave, lane, acc, acc_lane, etas[it], lam);
+            acc = 0;
+            if (!go || it + 1 == a.n_iters) break;
+            continue;
+        }
 
         s_acc[threadIdx.x] = acc_lane ? static_cast<u128>(acc) : static_cast<u128>(0);
         acc = 0;
@@ -919,18 +995,7 @@ __global__ __launch_bounds__(kBlockThreads, 2) void k_csr(KArgs a) {
             s_bsum[threadIdx.x] = v;
         }
         __syncthreads();
-        if constexpr (Mode == kResident) {
-            if (a.nblk == 1) {
-                finish_cluster<R, false>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_stop);
-                if (it + 1 == a.n_iters) break;
-                if (!next_prices_local<R>(s_lam, s_newlam, &s_stop)) break;
-            } else {
-                if (!exchange_iteration<R>(ai, cl, blk, s_bsum, s_lam, s_newlam, &s_go)) break;
-                if (it + 1 == a.n_iters) break;
-                if (threadIdx.x < R) s_lam[threadIdx.x] = s_newlam[threadIdx.x];
-                __syncthreads();
-            }
-        } else if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
+        if (Mode == kPersistDeferred || (Mode == kOnePass && a.defer)) {
             publish_iteration<R, Mode == kPersistDeferred>(ai, cl, blk, ai.iter_no, s_bsum);
             if (Mode == kOnePass || it + 1 == a.n_iters) break;    // the next launch completes it
             load_tile(min(tile0, last), rev ^ a.sweep_alt, nu, nd, npn, nhw);
