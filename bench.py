@@ -493,7 +493,9 @@ def _calibrate_stream(args, np, torch) -> int:
 def _kernel_sha() -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in ("esp_kernels.hip", "esp_device.hpp", "esp_internal.hpp"):
+    for f in ("esp_kernels.hpp", "esp_kernels.hip", "esp_device.hpp", "esp_internal.hpp", "esp_inst_dense12.hip",
+              "esp_inst_dense34.hip", "esp_inst_dense56.hip", "esp_inst_dense78.hip", "esp_inst_csr1234.hip",
+              "esp_inst_csr5678.hip"):
         h.update(open(os.path.join(ROOT, "paper_2608_07971_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
