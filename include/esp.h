@@ -136,11 +136,14 @@ typedef struct {
     int32_t reserved[4];             /* must be zero */
 } esp_options;
 
-/* esp_options.flags: also keep an entry-major copy of the table (each
- * configuration's utility and R demands contiguous, 4 (1 + R) bytes, so
- * B * nnz * 4 (1 + R) more workspace bytes) for esp_nearest_profile, which
- * then reads each job type's family as one contiguous run instead of a piece
- * of each of the 1 + R columns. */
+/* esp_options.flags: also keep an entry-major copy of the table for
+ * esp_nearest_profile, which then reads each job type's family as one
+ * contiguous run instead of a piece of each of the 1 + R columns.  Each
+ * configuration takes 4 (1 + R) bytes (its utility, then its R demands); each
+ * family's run starts on a 128-byte line, found through a directory of 64
+ * bytes per 60 job types.  More workspace: B * sum_j ceil(4 (1 + R) K_j / 128)
+ * * 128 bytes (about B * nnz * 4 (1 + R) plus 64 bytes per family) and
+ * 64 * ceil(N / 60) bytes. */
 #define ESP_OPT_PROFILE_STORE 1
 
 /* Optional per-iteration record of esp_solve (device pointers, iteration-major;

@@ -40,10 +40,11 @@ struct Plan {
     size_t col_len = 0; // floats per column
     int nblk = 0;       // workgroups per cluster
     int aos_stride = 0; // floats per entry of the entry-major copy, 0 when there is none
+    int64_t aos_lines = 0;  // kStoreLine-byte lines of one cluster's entry-major copy
     // workspace offsets (bytes)
     size_t o_table = 0, o_meta = 0, o_jobs = 0, o_shift = 0, o_cap = 0, o_eta = 0, o_part = 0,
            o_tick = 0, o_flags = 0, o_iters = 0, o_sync = 0, o_swc = 0, o_status = 0, o_capp = 0, o_offs = 0, o_inc = 0, o_gpus = 0,
-           o_aos = 0, o_lamws = 0, o_conv = 0, o_xch = 0, total = 0;
+           o_aos = 0, o_dir = 0, o_lamws = 0, o_conv = 0, o_xch = 0, total = 0;
     size_t columns() const { return static_cast<size_t>(R) + 1 + (pen ? 1 : 0); }
 };
 
@@ -57,6 +58,12 @@ int device_cus() {
 }
 
 bool dense_fast_k(int K) { return K == 4 || K == 8 || K == 16 || K == 32 || K == 64; }
+
+// Entry-major copy: lines of a family of k configurations, records of the directory.
+int64_t store_lines(int64_t k, int stride) {
+    return (k * stride * static_cast<int64_t>(sizeof(float)) + kStoreLine - 1) / kStoreLine;
+}
+int64_t dir_records(int N) { return (static_cast<int64_t>(N) + kDirFamilies - 1) / kDirFamilies; }
 
 // Family sizes of the problem (dense or CSR) and validation of the offsets.
 esp_status family_layout(const esp_problem *p, std::vector<int64_t> *sizes_out, int *uniform_k) {
@@ -167,8 +174,19 @@ esp_status make_plan(const esp_problem *p, const esp_options *opt, Plan *pl) {
     pl->o_offs = o;  o = align_up(o + (static_cast<size_t>(pl->N) + 1) * sizeof(int64_t));
     pl->o_inc = o;   o = align_up(o + B * static_cast<size_t>(pl->N) * sizeof(uint64_t));
     pl->o_gpus = o;  o = align_up(o + B * sizeof(int32_t));
-    if (opt && (opt->flags & ESP_OPT_PROFILE_STORE)) pl->aos_stride = pl->R + 1;
-    pl->o_aos = o;   o = align_up(o + B * static_cast<size_t>(pl->nnz) * pl->aos_stride * sizeof(float));
+    size_t dir_bytes = 0;
+    if (opt && (opt->flags & ESP_OPT_PROFILE_STORE)) {
+        pl->aos_stride = pl->R + 1;
+        int64_t lines = 0;
+        for (int j = 0; j < pl->N; ++j)
+            lines += store_lines(p->family_offsets ? p->family_offsets[j + 1] - p->family_offsets[j]
+                                                   : p->configs_per_job, pl->aos_stride);
+        if (lines > static_cast<int64_t>(UINT32_MAX)) return ESP_ERR_SHAPE;   // 32-bit line numbers
+        pl->aos_lines = lines;
+        dir_bytes = static_cast<size_t>(dir_records(pl->N)) * kDirWords * sizeof(uint32_t);
+    }
+    pl->o_aos = o;   o = align_up(o + B * static_cast<size_t>(pl->aos_lines) * kStoreLine);
+    pl->o_dir = o;   o = align_up(o + dir_bytes);
     pl->o_lamws = o; o = align_up(o + 2 * B * R * sizeof(double));
     pl->o_conv = o;  o = align_up(o + B * sizeof(int32_t));
     pl->o_xch = o;   o = align_up(o + 2 * B * pl->nblk * R * kMaxLimbs * sizeof(uint64_t));
@@ -638,6 +656,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     std::vector<TileMeta> meta;
     std::vector<JobSlot> jobs;
     std::vector<int64_t> slot_of(N);
+    std::vector<uint32_t> dir;          // directory of the entry-major copy (copied on `s` below)
     if (pl.csr) {
         meta.assign(pl.tiles, TileMeta{});
         jobs.resize(N);
@@ -660,7 +679,7 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
     }
     {
         PinnedPair pp;
-        pp.cap = pl.col_len;
+        pp.cap = std::max<size_t>(pl.col_len, store_lines(kMaxFamily, kMaxR + 1) * kStoreLine / sizeof(float));   // a column, or the longest family run
         for (int i = 0; i < 2; ++i) {
             if (hipHostMalloc(reinterpret_cast<void **>(&pp.buf[i]), sizeof(float) * pp.cap) != hipSuccess)
                 return fail(ESP_ERR_DEVICE);
@@ -707,38 +726,75 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                 which ^= 1;
             }
         }
-        // Entry-major copy (ESP_OPT_PROFILE_STORE): entry e of cluster b holds
-        // its utility (-inf when masked), then its R demands.
+        // Entry-major copy (ESP_OPT_PROFILE_STORE): family j of cluster b is a
+        // run of slots of 1 + R floats (the utility, -inf when masked, then
+        // the R demands) starting on a kStoreLine-byte line; the slots after
+        // its last configuration, up to the end of its last line, are masked
+        // entries.  Whole families are staged, then copied.
         if (pl.aos_stride > 0) {
-            const size_t stride = static_cast<size_t>(pl.aos_stride);
-            const size_t per_chunk = std::max<size_t>(1, pp.cap / stride);
+            const size_t st = static_cast<size_t>(pl.aos_stride);
+            constexpr size_t kLineFloats = kStoreLine / sizeof(float);
+            float *dst0 = reinterpret_cast<float *>(ws + pl.o_aos);
+            float *h = nullptr;
+            size_t n = 0, out = 0;                      // floats staged in h; floats of the copy written
+            auto flush = [&]() -> bool {
+                if (n > 0) {
+                    if (hipMemcpyAsync(dst0 + out, h, sizeof(float) * n, hipMemcpyHostToDevice, s) != hipSuccess ||
+                        hipEventRecord(pp.ev[which], s) != hipSuccess)
+                        return false;
+                    pp.pending[which] = true;
+                    which ^= 1;
+                    out += n;
+                }
+                h = nullptr;
+                n = 0;
+                return true;
+            };
             for (int b = 0; b < B; ++b) {
                 const float *u = p->utility + static_cast<size_t>(b) * nnz;
                 const float *d = p->demand + static_cast<size_t>(b) * nnz * R;
                 const uint8_t *f = p->feasible ? p->feasible + static_cast<size_t>(b) * nnz : nullptr;
-                for (size_t e0 = 0; e0 < static_cast<size_t>(nnz); e0 += per_chunk) {
-                    const size_t n = std::min(per_chunk, static_cast<size_t>(nnz) - e0);
-                    if (pp.pending[which]) {
-                        if (hipEventSynchronize(pp.ev[which]) != hipSuccess) return fail(ESP_ERR_DEVICE);
-                        pp.pending[which] = false;
+                for (int j = 0; j < N; ++j) {
+                    const int64_t e0 = off[j], k = off[j + 1] - off[j];
+                    const size_t fl = static_cast<size_t>(store_lines(k, pl.aos_stride)) * kLineFloats;
+                    if (h != nullptr && n + fl > pp.cap && !flush()) return fail(ESP_ERR_DEVICE);
+                    if (h == nullptr) {
+                        if (pp.pending[which]) {
+                            if (hipEventSynchronize(pp.ev[which]) != hipSuccess) return fail(ESP_ERR_DEVICE);
+                            pp.pending[which] = false;
+                        }
+                        h = pp.buf[which];
                     }
-                    float *h = pp.buf[which];
-                    std::fill(h, h + n * stride, 0.0f);
-                    for (size_t i = 0; i < n; ++i) {
-                        const size_t e = e0 + i;
-                        h[i * stride] = (f && f[e] == 0) ? neg_inf : u[e];
+                    float *run = h + n;
+                    std::fill(run, run + fl, 0.0f);
+                    for (size_t i = 0; i < fl / st; ++i) {
+                        float *slot = run + i * st;
+                        if (static_cast<int64_t>(i) >= k) {
+                            slot[0] = neg_inf;
+                            continue;
+                        }
+                        const size_t e = static_cast<size_t>(e0) + i;
+                        slot[0] = (f && f[e] == 0) ? neg_inf : u[e];
                         for (int r = 0; r < R; ++r) {
                             const float v = d[e * R + r];
-                            h[i * stride + 1 + r] = (v == 0.0f) ? 0.0f : v;
+                            slot[1 + r] = (v == 0.0f) ? 0.0f : v;     // -0.0 -> +0.0
                         }
                     }
-                    float *dst = reinterpret_cast<float *>(ws + pl.o_aos) + (static_cast<size_t>(b) * nnz + e0) * stride;
-                    if (hipMemcpyAsync(dst, h, sizeof(float) * n * stride, hipMemcpyHostToDevice, s) != hipSuccess ||
-                        hipEventRecord(pp.ev[which], s) != hipSuccess)
-                        return fail(ESP_ERR_DEVICE);
-                    pp.pending[which] = true;
-                    which ^= 1;
+                    n += fl;
                 }
+                if (!flush()) return fail(ESP_ERR_DEVICE);
+            }
+            // directory: first line of each group of kDirFamilies families, then
+            // each family's size - 1 (1..kMaxFamily configurations) in a byte
+            dir.assign(static_cast<size_t>(dir_records(N)) * kDirWords, 0u);
+            int64_t line = 0;
+            for (int j = 0; j < N; ++j) {
+                const int64_t k = off[j + 1] - off[j];
+                uint32_t *rec = dir.data() + static_cast<size_t>(j / kDirFamilies) * kDirWords;
+                const int i = j % kDirFamilies;
+                if (i == 0) rec[0] = static_cast<uint32_t>(line);
+                rec[1 + i / 4] |= static_cast<uint32_t>(k - 1) << (8 * (i % 4));
+                line += store_lines(k, pl.aos_stride);
             }
         }
         std::vector<double> cap(p->capacity, p->capacity + static_cast<size_t>(B) * R);
@@ -763,6 +819,9 @@ esp_status esp_create(const esp_problem *p, const esp_step_rule *step, const esp
                   hipMemcpyAsync(ws + pl.o_offs, off.data(), sizeof(int64_t) * off.size(), hipMemcpyHostToDevice,
                                  s) == hipSuccess &&
                   hipMemsetAsync(ws + pl.o_inc, 0, sizeof(uint64_t) * static_cast<size_t>(B) * N, s) == hipSuccess;
+        if (ok && !dir.empty())
+            ok = hipMemcpyAsync(ws + pl.o_dir, dir.data(), sizeof(uint32_t) * dir.size(), hipMemcpyHostToDevice,
+                                s) == hipSuccess;
         if (ok && pl.csr)
             ok = hipMemcpyAsync(ws + pl.o_meta, meta.data(), sizeof(TileMeta) * meta.size(), hipMemcpyHostToDevice,
                                 s) == hipSuccess &&
@@ -987,8 +1046,8 @@ esp_status esp_nearest_profile(esp_ctx *store, int32_t num_queries, const int32_
     na.Q = num_queries;
     const Plan &pl = store->pl;
     na.aos = pl.aos_stride > 0 ? reinterpret_cast<const float *>(store->ws + pl.o_aos) : nullptr;
-    na.offsets = reinterpret_cast<const int64_t *>(store->ws + pl.o_offs);
-    na.nnz = pl.nnz;
+    na.dir = reinterpret_cast<const uint32_t *>(store->ws + pl.o_dir);
+    na.aos_lines = pl.aos_lines;
     na.aos_stride = pl.aos_stride;
     return dev(launch_nearest(store->pl.R, store->base, na, static_cast<hipStream_t>(stream)));
 }

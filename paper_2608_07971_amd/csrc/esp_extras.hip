@@ -145,6 +145,16 @@ __global__ __launch_bounds__(kBlockThreads) void k_reserve(KArgs a, ReserveArgs 
 
 constexpr int kNearestLanes = 16;                     // lanes per query (one DPP row)
 
+// Sum over the 16 lanes of a DPP row, in every lane of the row.
+__device__ __forceinline__ uint32_t row_sum(uint32_t v) {
+    constexpr int kRowRor8 = 0x128, kRowRor4 = 0x124, kRowRor2 = 0x122, kRowRor1 = 0x121;
+    v += static_cast<uint32_t>(dpp_i<kRowRor8>(static_cast<int>(v)));
+    v += static_cast<uint32_t>(dpp_i<kRowRor4>(static_cast<int>(v)));
+    v += static_cast<uint32_t>(dpp_i<kRowRor2>(static_cast<int>(v)));
+    v += static_cast<uint32_t>(dpp_i<kRowRor1>(static_cast<int>(v)));
+    return v;
+}
+
 // Query i of a cluster names a job type f and an unprofiled configuration's
 // resource vector q.  The 16 lanes of one DPP row serve a query: lane s takes
 // entries s, s+16, ... of family f, skips masked ones (utility -inf), and
@@ -158,46 +168,94 @@ constexpr int kNearestLanes = 16;                     // lanes per query (one DP
 // records an error.
 //
 // The family is read from the store's entry-major copy (AOS: each entry's
-// utility and demands contiguous, so the family is one contiguous run) or
-// from the structure-of-arrays columns of the price loop's table.  The kernel
-// is bound by the dependent gathers (query -> family extent -> entries), not
-// by its arithmetic; keeping two queries per row in flight was measured
-// slower (fewer resident waves).
+// utility and demands contiguous, so the family is one contiguous run that
+// starts on a cache line) or from the structure-of-arrays columns of the
+// price loop's table.  With the copy, the row finds the run from the
+// directory record of the family's group of 60: lane 0 holds the group's
+// first line, lanes 1..15 hold four one-byte family sizes each, and two row
+// sums give the run's first line (the group's first line plus the lines of
+// the families before f) and the family's size.  The directory (64 bytes per
+// 60 families) stays in L2.
+//
+// Each query is a chain of dependent gathers (query -> family extent ->
+// entries), so a row works on three queries at once: while it reads the
+// entries of query i it has the extent of query i+1 and the family index of
+// query i+2 in flight, and every step waits for one memory round trip
+// instead of three.
 template <int R, bool AOS>
 __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs na) {
     constexpr int kPerBlock = kBlockThreads / kNearestLanes;
+    constexpr uint32_t kEntryBytes = 4 * (R + 1);
     const int sub = threadIdx.x & (kNearestLanes - 1);
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kPerBlock;
-    // every lane of a row shares gi, so rows stay whole for the DPP steps
-    for (int64_t gi = static_cast<int64_t>(blockIdx.x) * kPerBlock + threadIdx.x / kNearestLanes; gi < na.total;
-         gi += stride) {
-        const int f = na.family[gi];
-        float q[R];
-        bool ok = (f >= 0) & (f < a.N);
+    // The workgroup takes queries [lo, lo + chunk), kPerBlock at a time (one
+    // per row), so the cache lines of the query and output arrays it touches
+    // are its own.
+    constexpr int64_t stride = kPerBlock;
+    const int64_t lo = static_cast<int64_t>(blockIdx.x) * na.chunk;
+    const int64_t last = min(lo + na.chunk, na.total) - 1;
+    auto family_of = [&](int64_t g) { return na.family[g < last ? g : last]; };
+    auto query_of = [&](int64_t g, float (&v)[R]) {
+        const float *p = na.query + (g < last ? g : last) * R;
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            q[r] = na.query[gi * R + r];
-            ok = ok & (fabsf(q[r]) <= 3.402823466e38f);      // false for NaN and +-inf
+        for (int r = 0; r < R; ++r) v[r] = p[r];
+    };
+    auto in_range = [&](int f) { return (f >= 0) & (f < a.N); };
+    // The extent lookup of a family (any value: out-of-range ones read family 0).
+    // AOS: this lane's word of the family's directory record; else the family's
+    // slot and size in the columns.
+    auto extent_load = [&](int f) -> uint64_t {
+        const int fc = in_range(f) ? f : 0;
+        if constexpr (AOS) {
+            return na.dir[static_cast<size_t>(fc / kDirFamilies) * kDirWords + sub];
+        } else {
+            if (a.K > 0) return (static_cast<uint64_t>(a.K) << 32) | (static_cast<uint32_t>(fc) * static_cast<uint32_t>(a.K));
+            const JobSlot js = a.jobs[fc];
+            return (static_cast<uint64_t>(js.size) << 32) | js.slot;
         }
+    };
+    // every lane of a row shares gi, so rows stay whole for the DPP steps
+    int64_t gi = lo + threadIdx.x / kNearestLanes;
+    if (gi > last) return;
+    int f = family_of(gi);
+    float q[R];
+    query_of(gi, q);
+    uint64_t ext = extent_load(f);
+    int f1 = family_of(gi + stride);
+    for (; gi <= last; gi += stride) {
+        bool ok = in_range(f);
+#pragma unroll
+        for (int r = 0; r < R; ++r) ok = ok & (fabsf(q[r]) <= 3.402823466e38f);   // false for NaN and +-inf
+        // next steps of the pipeline: the query and extent of gi + stride, the family of gi + 2 stride
+        const uint64_t ext1 = extent_load(f1);
+        const int f2 = family_of(gi + 2 * stride);
+        float q1[R];
+        query_of(gi + stride, q1);
         int size = 0;
         const float *base = nullptr;       // the family's first entry (AOS) or its slot in column 0
-        if (ok) {
-            const int cl = static_cast<int>(gi / na.Q);
-            if constexpr (AOS) {
-                const int64_t e0 = na.offsets[f];
-                size = static_cast<int>(na.offsets[f + 1] - e0);
-                base = na.aos + (static_cast<size_t>(cl) * na.nnz + e0) * na.aos_stride;
-            } else {
-                uint32_t slot;
-                if (a.K > 0) {
-                    slot = static_cast<uint32_t>(f) * static_cast<uint32_t>(a.K);
-                    size = a.K;
-                } else {
-                    slot = a.jobs[f].slot;
-                    size = static_cast<int>(a.jobs[f].size);
+        const int cl = static_cast<int>(gi / na.Q);
+        if constexpr (AOS) {
+            const uint32_t w = static_cast<uint32_t>(ext);
+            const int i = (in_range(f) ? f : 0) % kDirFamilies;
+            const int first = 4 * (sub - 1);                 // family of byte 0 of this word
+            uint32_t before = w, own = 0;                    // lane 0: the group's first line
+            if (sub > 0) {
+                before = 0;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const uint32_t k = ((w >> (8 * m)) & 0xffu) + 1u;      // family size, 1..256
+                    if (first + m < i) before += (k * kEntryBytes + (kStoreLine - 1)) / kStoreLine;
+                    if (first + m == i) own = k;
                 }
-                base = a.table + cl * a.cluster_stride + slot;
             }
+            before = row_sum(before);
+            own = row_sum(own);
+            if (ok) {
+                size = static_cast<int>(own);
+                base = na.aos + (static_cast<size_t>(cl) * na.aos_lines + before) * (kStoreLine / 4);
+            }
+        } else if (ok) {
+            size = static_cast<int>(ext >> 32);
+            base = a.table + cl * a.cluster_stride + static_cast<uint32_t>(ext);
         }
         double best = -__builtin_inf();
         int bk = 0x7fffffff;
@@ -205,7 +263,7 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
         for (int k = sub; k < size; k += kNearestLanes) {
             float d[R + 1];                                  // utility, then the R demands
             if constexpr (AOS) {
-                __builtin_memcpy(d, base + static_cast<size_t>(k) * na.aos_stride, sizeof d);
+                __builtin_memcpy(d, base + static_cast<size_t>(k) * (R + 1), sizeof d);
             } else {
 #pragma unroll
                 for (int r = 0; r <= R; ++r) d[r] = base[r * a.col_len + k];
@@ -232,10 +290,15 @@ __global__ __launch_bounds__(kBlockThreads) void k_nearest(KArgs a, NearestArgs 
         if (sub == 0) {
             na.nearest[gi] = found ? bk : -1;
             if (na.estimate && !found) na.estimate[gi] = __builtin_nanf("");
-            if (!ok) atomicCAS(a.status, 0, (f >= 0 && f < a.N) ? kStatusNonfinite : kStatusInvalid);
+            if (!ok) atomicCAS(a.status, 0, in_range(f) ? kStatusNonfinite : kStatusInvalid);
         }
         // the entry's own lane (entries k of lane s satisfy k = s mod 16)
         if (found && na.estimate && mine == bk) na.estimate[gi] = bu;
+        f = f1;
+        ext = ext1;
+        f1 = f2;
+#pragma unroll
+        for (int r = 0; r < R; ++r) q[r] = q1[r];
     }
 }
 
@@ -606,13 +669,17 @@ __global__ void k_iac_reset(float *table, size_t cluster_stride, size_t col_len,
 template <int R>
 static hipError_t launch_nearest_r(const KArgs &a, const NearestArgs &na, hipStream_t s) {
     constexpr int kPerBlock = kBlockThreads / kNearestLanes;
-    const int64_t need = (na.total + kPerBlock - 1) / kPerBlock;
+    constexpr int64_t kLineQueries = 32;             // one 128-byte line of 4-byte outputs
     const int64_t cap = 256 * 32;                    // enough resident queries to cover gather latency
-    const dim3 grid(static_cast<unsigned>(need < cap ? need : cap)), block(kBlockThreads);
+    const int64_t need = (na.total + kPerBlock - 1) / kPerBlock;
+    NearestArgs nb = na;
+    nb.chunk = (na.total + (need < cap ? need : cap) - 1) / (need < cap ? need : cap);
+    nb.chunk = (nb.chunk + kLineQueries - 1) / kLineQueries * kLineQueries;
+    const dim3 grid(static_cast<unsigned>((na.total + nb.chunk - 1) / nb.chunk)), block(kBlockThreads);
     if (na.aos)
-        hipLaunchKernelGGL((k_nearest<R, true>), grid, block, 0, s, a, na);
+        hipLaunchKernelGGL((k_nearest<R, true>), grid, block, 0, s, a, nb);
     else
-        hipLaunchKernelGGL((k_nearest<R, false>), grid, block, 0, s, a, na);
+        hipLaunchKernelGGL((k_nearest<R, false>), grid, block, 0, s, a, nb);
     return hipGetLastError();
 }
 

@@ -27,15 +27,28 @@ struct NearestArgs {
     float *estimate;               // [B][Q] utility (throughput) of the nearest entry, or NULL
     int64_t total;                 // B * Q
     int32_t Q;                     // queries per cluster
-    // Entry-major copy of the store (ESP_OPT_PROFILE_STORE), or NULL: entry e
-    // of cluster b at aos + (b * nnz + e) * aos_stride, utility first, then
-    // the R demands; entries in the problem's order (family f = offsets[f]
-    // .. offsets[f+1] - 1).
+    int64_t chunk;                 // queries per workgroup (set by the launcher)
+    // Entry-major copy of the store (ESP_OPT_PROFILE_STORE), or NULL.  Each
+    // family is a run of slots of aos_stride floats (utility first, then the
+    // R demands; slot k = configuration k of the family) that starts on a
+    // kStoreLine-byte line; the slots after the family's last configuration,
+    // up to the end of its last line, hold masked entries (utility -inf, zero
+    // demands).  Cluster b's copy starts aos_lines lines after cluster b-1's.
     const float *aos;
-    const int64_t *offsets;        // [N+1]
-    int64_t nnz;
+    // Directory of the runs, shared by all clusters: one record of kDirWords
+    // words per kDirFamilies consecutive families.  Word 0 is the first line
+    // of the record's first family; family kDirFamilies g + i stores its size
+    // minus one at byte i of words 1..15 (byte i % 4 of word 1 + i / 4); its
+    // run takes ceil(size * 4 (1 + R) / kStoreLine) lines.
+    const uint32_t *dir;
+    int64_t aos_lines;             // lines per cluster
     int32_t aos_stride;            // floats per entry: 1 + R
 };
+
+constexpr int kStoreLine = 128;                     // bytes: the L2 line of gfx950
+constexpr int kDirWords = 16;                       // one 64-byte record
+constexpr int kDirFamilies = 4 * (kDirWords - 1);   // 60 sizes of one byte
+static_assert(kMaxFamily <= 256, "family sizes minus one fit a byte");
 
 // Outer ESP-IAC rounds (Alg. 1): one wavefront per cluster packs the
 // selection onto GPUs (first fit), evaluates co-located pairs and raises the

@@ -51,14 +51,18 @@ def test_workspace_size_dense_and_csr():
 
 
 def test_workspace_size_profile_store():
-    # the entry-major copy adds B * nnz * (1 + R) floats (plus alignment)
-    for inst in (workloads.make("tiny"), workloads.make("ragged", n_jobs=3000)):
+    # the entry-major copy: each family's run rounded up to whole 128-byte
+    # lines, B copies, plus a 64-byte directory record per 60 families (each
+    # region aligned to 256 bytes)
+    for inst in (workloads.make("tiny"), workloads.make("ragged", n_jobs=3000),
+                 workloads.random_small(3, 301, 70, 8, n_clusters=3)):
         p = esp.Problem.from_instance(inst)
         base = _ws(p)
         more = _ws(p, esp.esp_options(0, 0, 0, esp.ESP_OPT_PROFILE_STORE))
-        nnz = int(p.utility.shape[1])
-        extra = p.B * nnz * (p.R + 1) * 4
-        assert extra <= more - base <= extra + 256
+        sizes = np.diff(np.asarray(inst.offsets, np.int64))
+        lines = int(((sizes * 4 * (p.R + 1) + 127) // 128).sum())
+        extra = p.B * lines * 128 + 64 * (-(-p.N // 60))
+        assert extra <= more - base <= extra + 2 * 256
 
 
 @pytest.mark.parametrize("field,value,code", [

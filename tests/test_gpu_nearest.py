@@ -69,7 +69,20 @@ STORES = {
     "dense_k16_r5": lambda: workloads.random_small(24, 500, 16, 5, dense=True, n_clusters=2),
     "dense_k64_r8": lambda: _masked(workloads.random_small(25, 200, 64, 8, dense=True), 2),
     "tiny": lambda: workloads.make("tiny"),
+    "csr_r8_long_families": lambda: _long_families(27, 8),
+    "csr_r2_long_families": lambda: _long_families(28, 2),
 }
+
+
+def _long_families(seed, R):
+    """Families from 1 to 256 configurations (the longest runs of the
+    entry-major copy: 72 lines at R = 8), sizes that fill whole lines, more
+    job types than one directory record holds."""
+    rng = np.random.default_rng(seed)
+    sizes = rng.choice([1, 2, 31, 32, 33, 64, 127, 128, 255, 256], 185)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    nnz = int(off[-1])
+    return store_instance(off, rng.random(nnz), rng.random((nnz, R)).astype(np.float32))
 
 
 def _masked(inst, seed):
