@@ -744,21 +744,16 @@ __device__ __forceinline__ unsigned below_lane(uint64_t m, unsigned acc) {
                                      __builtin_amdgcn_mbcnt_lo(static_cast<unsigned>(m), acc));
 }
 
-// One step of an inclusive segmented scan over lanes of (best score, slot,
+// One step of an inclusive segmented max-scan over lanes of (best score,
 // segment-start flag): a lane without a segment start combines the value
-// arriving from lower lanes.  That value covers only slots below the lane's
-// own range, so on equal scores it is the one kept: the lowest slot wins, as
-// in the sequential scan, with no comparison of slots.  A lane with no source
-// receives its own (score, slot) and a clear flag, which changes nothing.
+// arriving from lower lanes.  A lane with no source receives its own score
+// and a clear flag, which changes nothing.
 template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
+__device__ __forceinline__ void seg_scan_step(double &s, int &f) {
     const double os = dpp_or_d<CTRL, ROW_MASK>(s, s);
-    const int ok = dpp_or_i<CTRL, ROW_MASK>(k, k);
     const int of = dpp_or_i<CTRL, ROW_MASK>(0, f);
     // selects and bitwise operators, not branches (the lanes diverge on f)
-    const bool take = (f == 0) & (os >= s);
-    s = take ? os : s;
-    k = take ? ok : k;
+    s = ((f == 0) & (os > s)) ? os : s;
     f = f | of;
 }
 
@@ -770,7 +765,6 @@ __device__ __forceinline__ void seg_scan_step(double &s, int &k, int &f) {
 template <int R, typename A, int Mode>
 __global__ __launch_bounds__(kBlockThreads, Mode == kResident ? 1 : 2) void k_csr(KArgs a) {
     constexpr int Q = kWaveSize / R;           // accumulating lanes per resource
-    __shared__ uint32_t s_win[kBlockWaves][8];
     __shared__ float s_stage[kBlockWaves][kTileEntries][R];
     __shared__ u128 s_acc[kBlockThreads];
     __shared__ u128 s_wsum[kBlockWaves][R];
@@ -798,6 +792,7 @@ __global__ __launch_bounds__(kBlockThreads, Mode == kResident ? 1 : 2) void k_cs
     const float *col = a.table + cl * a.cluster_stride;
     const size_t lane_off = static_cast<size_t>(lane) * 4;
     const int hshift = (lane & 7) * 4;                   // this lane's 4 head bits in its word
+    const uint64_t above = lane == kWaveSize - 1 ? 0ull : ~0ull << (lane + 1);   // the lanes above this one
     const double sw = a.has_pen ? a.switch_cost[cl] : 0.0;
     const int stride = a.nblk * kBlockWaves;
     const int last = a.tiles - 1;
@@ -856,35 +851,34 @@ __global__ __launch_bounds__(kBlockThreads, Mode == kResident ? 1 : 2) void k_cs
         }
         const bool has_head = hbits != 0;
         const bool has_pre = has_head & !h0;
-        const int pre_k = lane * 4 + pre_i;
+        // Segment maxima across lanes: after the scan, ps is the largest score
+        // of the segment open at this lane's end, over its slots up to here.
         double ps = run_s;
-        int pk = lane * 4 + run_i;
         int pf = has_head ? 1 : 0;
-        seg_scan_step<kDppRowShr1, 0xf>(ps, pk, pf);
-        seg_scan_step<kDppRowShr2, 0xf>(ps, pk, pf);
-        seg_scan_step<kDppRowShr4, 0xf>(ps, pk, pf);
-        seg_scan_step<kDppRowShr8, 0xf>(ps, pk, pf);
-        seg_scan_step<kDppRowBcast15, 0xa>(ps, pk, pf);
-        seg_scan_step<kDppRowBcast31, 0xc>(ps, pk, pf);
-        // Value of the scan at the previous lane (the segment that ends inside this lane).
+        seg_scan_step<kDppRowShr1, 0xf>(ps, pf);
+        seg_scan_step<kDppRowShr2, 0xf>(ps, pf);
+        seg_scan_step<kDppRowShr4, 0xf>(ps, pf);
+        seg_scan_step<kDppRowShr8, 0xf>(ps, pf);
+        seg_scan_step<kDppRowBcast15, 0xa>(ps, pf);
+        seg_scan_step<kDppRowBcast31, 0xc>(ps, pf);
+        // the same at the previous lane (lane 0: its own value)
         const double qs = dpp_or_d<kDppWaveShr1, 0xf>(ps, ps);
-        int qk = dpp_or_i<kDppWaveShr1, 0xf>(pk, pk);
-
-        // Winner mask of the tile (one bit per slot), built in LDS.
-        if (lane < 8) s_win[wave][lane] = 0u;
-        wave_sync();
-        if (local_win) atomicOr(&s_win[wave][lane >> 3], local_win << hshift);
-        if (has_head & (lane > 0)) {
-            // the segment's part in this lane (before the first head) has the
-            // higher slots: it wins only with a strictly larger score
-            qk = (has_pre & (pre_s > qs)) ? pre_k : qk;
-            atomicOr(&s_win[wave][(qk >> 5) & 7], 1u << (qk & 31));
-        }
-        if (lane == kWaveSize - 1) atomicOr(&s_win[wave][(pk >> 5) & 7], 1u << (pk & 31));
-        wave_sync();
-        const uint32_t my_word = s_win[wave][lane >> 3];
-        wave_sync();
-        const uint32_t wbits = (my_word >> hshift) & 0xFu;
+        // Each winner is marked by the lane that holds it.  The winner of a
+        // segment is its first slot with the segment's largest score: in the
+        // lane where the running maximum last rose (a head, or a run strictly
+        // above everything before it: lane `jump`), its run's best, unless the
+        // part of the next head lane before its first head (slots above all
+        // of the segment's others) beats it strictly (`pre_wins` there).
+        const bool jump = has_head | (ps > qs) | (lane == 0);
+        const bool pre_wins = has_pre & (pre_s > qs);
+        const uint64_t m_head = __ballot(has_head);
+        const uint64_t m_rise = __ballot(jump);
+        const uint64_t m_keep = m_head & ~__ballot(pre_wins);   // head lanes whose pre part loses
+        // the next lane above this one where the maximum rises or a segment starts
+        const uint64_t later = m_rise & above;
+        const int nxt = later ? __builtin_ctzll(later) : kWaveSize;
+        const bool run_wins = jump & ((nxt == kWaveSize) | (((m_keep >> (nxt & (kWaveSize - 1))) & 1ull) != 0ull));
+        const uint32_t wbits = local_win | (pre_wins ? 1u << pre_i : 0u) | (run_wins ? 1u << run_i : 0u);
         // Rank of this lane's first winner among the tile's winners (slot
         // order: lane, then entry): the winners in lower lanes, counted from
         // one ballot per entry position; n_win is the same for every lane.
